@@ -1,0 +1,200 @@
+"""Pins that tie the CPU oracle to things other than itself.
+
+Every check takes a loaded oracle library (ctypes CDLL exposing rg_oracle_dot
+and rg_oracle_linear), so the same checks run against the real oracle and
+against deliberately broken copies of it (tests/test_oracle_mutants.py).
+Each check returns a list of failure strings (empty = pass).
+
+What pins what:
+  * hand-derived probes (tests/golden/order_probes.json): the segment length,
+    the in-segment sequential order, the left fold, the +0 start, subnormals;
+  * binary64 reference within gamma_n * sum|x*w| (Higham's inner-product
+    bound): no dropped, doubled or misplaced term, on many ragged K;
+  * integer-valued inputs: every order gives the exact integer, so a wrong
+    operand pairing, transposition or index shows up as a wrong integer;
+  * exact-rational emulation of binary32 FMA and addition on tiny inputs:
+    correct rounding, signed zeros and gradual underflow of the C library;
+  * invariants: rows of x and of W permute outputs; a batch is its rows.
+"""
+import ctypes
+import json
+import os
+import struct
+
+import numpy as np
+
+from tests import fp32_exact as fx
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "order_probes.json")
+CHUNK = 256
+U32 = 2.0 ** -24
+
+
+def _setup(L):
+    vp, i64, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    L.rg_oracle_dot.argtypes = [vp, vp, i64]
+    L.rg_oracle_dot.restype = ctypes.c_float
+    L.rg_oracle_linear.argtypes = [vp, vp, vp, i64, i64, i64, ci]
+    L.rg_oracle_linear.restype = ci
+    return L
+
+
+def _linear(L, x, w, nthreads=4):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    M, K = x.shape
+    N = w.shape[0]
+    y = np.empty((M, N), dtype=np.float32)
+    rc = L.rg_oracle_linear(x.ctypes.data, w.ctypes.data, y.ctypes.data, M, N, K, nthreads)
+    assert rc == 0
+    return y
+
+
+def f32_bits(v) -> int:
+    return struct.unpack("<I", struct.pack("<f", float(v)))[0]
+
+
+def load_probes():
+    with open(GOLDEN) as f:
+        return json.load(f)["probes"]
+
+
+def probe_inputs(p):
+    K = p["K"]
+    x = np.zeros((1, K), dtype=np.float32)
+    w = np.full((1, K), 0x3F80, dtype=np.uint16)
+    for a, b, v in p["x"]:
+        x[0, a:b] = float.fromhex(v)
+    for a, b, v in p.get("w", []):
+        w[0, a:b] = int(v, 16)
+    return x, w
+
+
+def check_probes(L):
+    L = _setup(L)
+    fails = []
+    for p in load_probes():
+        x, w = probe_inputs(p)
+        got = f32_bits(_linear(L, x, w)[0, 0])
+        want = int(p["expect_bits"], 16)
+        if got != want:
+            fails.append(f"{p['name']}: got 0x{got:08x} want 0x{want:08x}")
+    return fails
+
+
+def gamma(K):
+    J = -(-K // CHUNK)
+    n = min(CHUNK, K) + J - 1
+    return n * U32 / (1.0 - n * U32)
+
+
+def check_fp64_bound(L, Ks=None, seed=0):
+    """|y - y64| <= gamma_n * sum|x w| (+ the binary64 sum's own error) on ragged K."""
+    L = _setup(L)
+    rng = np.random.default_rng(seed)
+    if Ks is None:
+        Ks = [1, 2, 7, 8, 9, 100, 255, 256, 257, 300, 511, 512, 513, 600, 1000, 1024, 1500, 2048, 4100]
+    fails = []
+    for K in Ks:
+        M, N = 3, 5
+        x = rng.standard_normal((M, K)).astype(np.float32)
+        wf = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+        w = (wf.view(np.uint32) >> 16).astype(np.uint16)    # truncation is fine for inputs
+        y = _linear(L, x, w).astype(np.float64)
+        wv = (w.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+        prod = x.astype(np.float64)[:, None, :] * wv[None, :, :]           # exact in binary64
+        y64 = prod.sum(axis=2)
+        a = np.abs(prod).sum(axis=2)
+        g64 = K * 2.0 ** -53 / (1 - K * 2.0 ** -53)
+        bound = gamma(K) * a + g64 * a
+        err = np.abs(y - y64)
+        if not np.all(err <= bound):
+            i = np.unravel_index(np.argmax(err - bound), err.shape)
+            fails.append(f"K={K}: |y-y64|={err[i]:.3e} > bound {bound[i]:.3e}")
+    return fails
+
+
+def check_integer_exact(L):
+    """Small integers: all partial sums are exact, so y is the integer dot product in any order."""
+    L = _setup(L)
+    fails = []
+    for (M, N, K) in [(3, 4, 5), (2, 7, 256), (4, 3, 257), (5, 6, 700), (1, 9, 1000)]:
+        m = np.arange(M)[:, None]
+        n = np.arange(N)[:, None]
+        k = np.arange(K)[None, :]
+        xi = ((3 * m + k) % 7) - 3
+        wi = ((n + 2 * k) % 5) - 2
+        x = xi.astype(np.float32)
+        w = (wi.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)   # exact in bf16
+        want = xi.astype(np.int64) @ wi.astype(np.int64).T
+        got = _linear(L, x, w)
+        if not np.array_equal(got.astype(np.int64), want) or not np.all(got == want):
+            fails.append(f"integer-exact ({M},{N},{K}) mismatch")
+    return fails
+
+
+def emulated_dot(xr, wr):
+    """The documented order on exact rationals: segment chains of fma, then a left fold."""
+    K = len(xr)
+    y = None
+    for k0 in range(0, K, CHUNK):
+        p = 0.0
+        for k in range(k0, min(k0 + CHUNK, K)):
+            p = fx.fma(float(xr[k]), fx.bf16_to_float(int(wr[k])), p)
+        y = p if y is None else fx.add(y, p)
+    return y
+
+
+def check_exact_emulation(L, seed=1):
+    """Tiny random and adversarial rows: oracle bits == exact-rational emulation bits."""
+    L = _setup(L)
+    rng = np.random.default_rng(seed)
+    fails = []
+    cases = []
+    for K in (1, 3, 17, 256, 257, 520):
+        x = rng.standard_normal(K).astype(np.float32)
+        w = ((rng.standard_normal(K) * 0.02).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        cases.append((f"normal K={K}", x, w))
+    # wide dynamic range with subnormal products and cancellations
+    K = 300
+    x = (rng.standard_normal(K) * 2.0 ** rng.integers(-70, 40, K)).astype(np.float32)
+    w = ((rng.standard_normal(K) * 2.0 ** rng.integers(-80, 10, K)).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    cases.append(("wide range", x, w))
+    x = np.array([1e-30, -1e-30, 3.0, -3.0] * 80, dtype=np.float32)
+    w = np.array([0x0001, 0x8001, 0x3F80, 0x3F80] * 80, dtype=np.uint16)
+    cases.append(("subnormal weights, cancellation", x, w))
+    for name, x, w in cases:
+        got = f32_bits(L.rg_oracle_dot(np.ascontiguousarray(x).ctypes.data, np.ascontiguousarray(w).ctypes.data, len(x)))
+        want = f32_bits(emulated_dot(x, w))
+        if got != want:
+            fails.append(f"{name}: got 0x{got:08x} want 0x{want:08x}")
+    return fails
+
+
+def check_invariants(L, seed=2):
+    """Row permutations of x and W permute y; a batch equals its rows computed alone."""
+    L = _setup(L)
+    rng = np.random.default_rng(seed)
+    M, N, K = 6, 7, 777
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    w = ((rng.standard_normal((N, K)) * 0.02).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    y = _linear(L, x, w)
+    fails = []
+    pm, pn = rng.permutation(M), rng.permutation(N)
+    yp = _linear(L, x[pm], w[pn])
+    if not np.array_equal(yp.view(np.uint32), y[pm][:, pn].view(np.uint32)):
+        fails.append("row permutation changed bits")
+    for m in range(M):
+        y1 = _linear(L, x[m:m + 1], w)
+        if not np.array_equal(y1.view(np.uint32), y[m:m + 1].view(np.uint32)):
+            fails.append(f"row {m} alone differs from the batch")
+    return fails
+
+
+ALL_CHECKS = {
+    "probes": check_probes,
+    "fp64_bound": check_fp64_bound,
+    "integer_exact": check_integer_exact,
+    "exact_emulation": check_exact_emulation,
+    "invariants": check_invariants,
+}
