@@ -1,0 +1,158 @@
+/*
+ * rg.h -- C-ABI of a bit-reproducible fused-upcast linear layer for AMD MI355X (gfx950).
+ *
+ * The operation (paper: Design, eq. 2, with the bias term left out):
+ *
+ *     y[m][n] = sum over k of  x[m][k] * up(W[n][k])
+ *
+ *   x : float32  [M][K] row-major (activations; the paper's FP32 compute path)
+ *   W : bfloat16 [N][K] row-major, passed as uint16_t bit patterns
+ *       (the nn.Linear [out][in] layout; weights stay resident in BF16)
+ *   y : float32  [M][N] row-major, fully overwritten (never read)
+ *
+ * up(b) widens a bfloat16 pattern to float32 exactly: the float whose bits are
+ * (uint32_t)b << 16.  It happens in registers; no FP32 copy of W is ever
+ * written to memory (Design, eq. 2 and the dataflow figure).
+ *
+ * THE REDUCTION ORDER ("RG-ORDER-1").  For every output element, with C = 256
+ * and J = ceil(K / C):
+ *
+ *   p_j = +0.0f;  for k = j*C .. min(j*C + C, K) - 1 in ascending order:
+ *                      p_j = fmaf(x[m][k], up(W[n][k]), p_j)
+ *   y   = p_0;    for j = 1 .. J-1 in ascending order:  y = y + p_j
+ *
+ * - Every multiply-add is one IEEE-754 binary32 fused multiply-add and every
+ *   combine one binary32 addition, round to nearest even, subnormals kept on
+ *   input and output (rule R1: IEEE FMA only; no matrix cores are used).
+ * - K is cut into fixed 256-wide segments (a pure function of K, rule R3);
+ *   each segment is one sequential chain in ascending k; the segment partials
+ *   are combined in fixed ascending segment order with no atomics (rule R3).
+ * - The order depends on K alone: not on M, N, the row m or n, the kernel
+ *   chosen, the grid, the block, the number of compute units, CU masks, the
+ *   stream or timing (rules R2 and R4).  A row of y is therefore bitwise the
+ *   same at every batch size M (batch invariance, rule R4, here for all M).
+ *
+ * Results are bitwise equal to the plain C CPU implementation of this order.
+ *
+ * Threading and streams.  Calls are asynchronous and stream ordered on the
+ * given stream (a hipStream_t passed as void*; NULL = the null stream).  The
+ * library never synchronizes and allocates no device memory in rg_linear.
+ * Concurrent calls on different streams are safe.  rg_linear_set_launch is
+ * process global and not thread safe (a test knob).
+ *
+ * Errors.  Every entry point returns an rg_status code; none aborts or prints.
+ */
+#ifndef RG_H
+#define RG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RG_CHUNK 256     /* segment length C of RG-ORDER-1 */
+#define RG_ORDER_ID 1    /* identifies RG-ORDER-1 in rg_plan_t.order_id */
+
+typedef enum {
+    RG_OK = 0,
+    RG_ERR_INVAL = 1,    /* null pointer, M/N/K < 1, or M*K, N*K, M*N overflow int64 */
+    RG_ERR_ALIGN = 2,    /* x, W or y not 4-byte aligned (W: 2-byte) */
+    RG_ERR_ARCH = 3,     /* current device is not gfx950 */
+    RG_ERR_HIP = 4,      /* a HIP runtime call failed (launch or query) */
+    RG_ERR_RANGE = 5,    /* an rg_launch_t field is out of its documented range */
+    RG_ERR_ALIAS = 6     /* y overlaps x or W */
+} rg_status;
+
+/* Kernel ids reported by rg_plan (scheduling only; the order is the same). */
+typedef enum {
+    RG_KERNEL_GENERIC = 0,   /* one thread per output; any K, any alignment */
+    RG_KERNEL_DECODE = 1,    /* M <= 8: quad-broadcast streaming GEMV, whole K per workgroup */
+    RG_KERNEL_TILED = 2      /* M > 8: register-tiled kernel, whole K per workgroup */
+} rg_kernel_id;
+
+/* Scheduling overrides for the determinism tests.  0 in a field = planner
+ * default.  None of these can change a result bit; they only move work
+ * between workgroups, waves and compute units.
+ *   kernel        : -1/0 = planner's choice, else 1 + rg_kernel_id to force one
+ *                   (a kernel that cannot handle the shape is not forced; the
+ *                    call returns RG_ERR_RANGE)
+ *   waves_per_wg  : 1..8  waves (64 threads each) per workgroup
+ *   grid_wgs      : 1..65536 workgroups (work is spread over them evenly)
+ *   depth         : 1..4  decode pipeline depth in 128-byte-per-row slabs
+ *   grid_order    : 0 = forward, 1 = reversed workgroup-to-rows mapping
+ */
+typedef struct {
+    int32_t kernel;
+    int32_t waves_per_wg;
+    int32_t grid_wgs;
+    int32_t depth;
+    int32_t grid_order;
+    int32_t reserved[3];
+} rg_launch_t;
+
+/* What rg_linear will do for a shape (on a 256-CU MI355X with default launch). */
+typedef struct {
+    int32_t order_id;      /* RG_ORDER_ID */
+    int32_t chunk;         /* C = 256 */
+    int64_t nchunks;       /* J = ceil(K / 256) */
+    int32_t kernel;        /* rg_kernel_id */
+    int32_t waves_per_wg;
+    int32_t grid_wgs;
+    int32_t depth;
+    int32_t rows_per_round;/* decode: W rows per workgroup round */
+    int32_t tile_m, tile_n;/* tiled: output tile */
+} rg_plan_t;
+
+/*
+ * y = x * up(W)^T in RG-ORDER-1 (Design, eq. 2; rules R1-R4).
+ *   x      device pointer, float32 [M][K], 4-byte aligned
+ *   w_bf16 device pointer, bfloat16 bits [N][K], 2-byte aligned
+ *   y      device pointer, float32 [M][N], 4-byte aligned, must not overlap x or W
+ *   M,N,K  >= 1
+ *   stream hipStream_t or NULL
+ * The caller owns all buffers.  Fast paths need 16-byte aligned x and W and
+ * K % 8 == 0; other shapes take a slower kernel with the same order and bits.
+ * Returns RG_OK once the kernel is enqueued, or an rg_status error (nothing
+ * is enqueued on error).  Launch-time HIP errors are returned as RG_ERR_HIP.
+ */
+int rg_linear(const float* x, const uint16_t* w_bf16, float* y, int64_t M, int64_t N, int64_t K,
+              void* stream);
+
+/* Set (cfg != NULL) or reset (cfg == NULL) the scheduling overrides used by
+ * later rg_linear calls.  RG_ERR_RANGE if a field is out of range. */
+int rg_linear_set_launch(const rg_launch_t* cfg);
+
+/* Fill *out with the plan for (M, N, K) under the current overrides.  A pure
+ * function of its arguments and the overrides; queries no device.  CPU safe. */
+int rg_plan(int64_t M, int64_t N, int64_t K, rg_plan_t* out);
+
+/* Comparison point only (the scheme the paper improves on, Design, eq. 1):
+ * w_f32[n][k] = up(W[n][k]) written to a caller-provided FP32 buffer of N*K
+ * floats (the transient copy the fused kernel never makes).  Any FP32 GEMM
+ * can then consume it.  Stream ordered, asynchronous. */
+int rg_cast_bf16_f32(const uint16_t* w_bf16, float* w_f32, int64_t count, void* stream);
+
+/* Greedy decision over logits (Evaluation, end-to-end determinism: argmax
+ * returns the lower token id on a tie): out_idx[m] = the lowest n with
+ * y[m][n] maximal, NaN never wins (all-NaN rows give -1).  y: device float32
+ * [M][N]; out_idx: device int64 [M].  Deterministic; no atomics. */
+int rg_argmax_rows(const float* y, int64_t* out_idx, int64_t M, int64_t N, void* stream);
+
+/* Test helpers: a stream restricted to the compute units set in `mask`
+ * (bit i of word i/32 = CU i), and its destruction. */
+int rg_stream_create_cu_mask(const uint32_t* mask, uint32_t nwords, void** out_stream);
+int rg_stream_destroy(void* stream);
+
+/* Number of compute units of the current device (RG_ERR_HIP if none). */
+int rg_device_cu_count(int32_t* out);
+
+/* Static description of an rg_status code (never NULL). */
+const char* rg_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RG_H */

@@ -1,0 +1,280 @@
+// C-ABI of the fused-upcast linear layer: argument checks, the shape-only
+// planner and kernel dispatch.  See include/rg.h for the contract.
+//
+// The planner decides only scheduling (which kernel, how many waves and
+// workgroups).  The floating-point order of every output is fixed by K alone
+// (paper: rules R2 and R3: configurations are a pure function of the shape,
+// the segmentation a pure function of K), and every kernel implements it.
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+
+#include "../../include/rg.h"
+#include "rg_kernels.h"
+
+namespace {
+
+constexpr int kNominalCUs = 256;            // MI355X; scheduling only
+constexpr int kMaxDevices = 64;
+constexpr int64_t kMaxDecodeRowsStage = 4096 / 4 * 4;  // rows * MT floats staged per WG <= 16 KB
+
+rg_launch_t g_launch = {};                  // all zero: planner defaults
+std::mutex g_launch_mu;
+
+struct DeviceInfo {
+    std::once_flag once;
+    int status = RG_OK;
+    int cus = 0;
+};
+DeviceInfo g_dev[kMaxDevices];
+
+int device_check(int* cus_out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return RG_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return RG_ERR_HIP;
+    DeviceInfo& d = g_dev[dev];
+    std::call_once(d.once, [&] {
+        hipDeviceProp_t p;
+        if (hipGetDeviceProperties(&p, dev) != hipSuccess) {
+            d.status = RG_ERR_HIP;
+            return;
+        }
+        d.cus = p.multiProcessorCount;
+        d.status = (std::strncmp(p.gcnArchName, "gfx950", 6) == 0) ? RG_OK : RG_ERR_ARCH;
+    });
+    if (cus_out) *cus_out = d.cus;
+    return d.status;
+}
+
+bool mul_ok(int64_t a, int64_t b) { return a <= 0 || b <= INT64_MAX / 4 / a; }
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+struct Plan {
+    int kernel = RG_KERNEL_GENERIC;
+    int mt = 0, nw = 0, grid = 0, depth = 0, rq = 0, reverse = 0;
+    int64_t Q = 0;
+    int max_rows_wg = 0;
+    int tile_m = 0, tile_n = 0;
+};
+
+// Decode schedule for a shape: waves per workgroup and quads per round.
+// Minimises rounds per workgroup, then idle lanes, then prefers more waves.
+bool decode_schedule(int64_t N, int64_t J, int mt, const rg_launch_t& o, Plan* p) {
+    static const int kNW[] = {7, 6, 4, 2, 1};
+    p->Q = ceil_div(N, 4);
+    int64_t grid = o.grid_wgs > 0 ? o.grid_wgs : (p->Q >= kNominalCUs ? kNominalCUs : p->Q);
+    // staging of results: 4 * ceil(Q/grid) rows * mt floats must stay small
+    while (4 * ceil_div(p->Q, grid) * mt > kMaxDecodeRowsStage) {
+        if (o.grid_wgs > 0) return false;
+        grid *= 2;
+    }
+    if (grid > p->Q) grid = p->Q;
+    const int64_t qpw = ceil_div(p->Q, grid);
+    int best_nw = 0, best_rq = 0;
+    int64_t best_rounds = 0;
+    double best_eff = -1.0;
+    for (int nw : kNW) {
+        if (o.waves_per_wg > 0 && nw != o.waves_per_wg) continue;
+        if (mt == 4 && nw > 4) continue;   // 4 rows of x need one wave per SIMD (registers)
+        const int64_t rq = (16 * nw) / J;
+        if (rq < 1) continue;
+        const int64_t rounds = ceil_div(qpw, rq);
+        const double eff = (double)(qpw * J) / (double)(rounds * 16 * nw);
+        const bool better = best_nw == 0 || rounds < best_rounds ||
+                            (rounds == best_rounds && eff > best_eff + 1e-9);
+        if (better) {
+            best_nw = nw;
+            best_rq = (int)rq;
+            best_rounds = rounds;
+            best_eff = eff;
+        }
+    }
+    if (best_nw == 0) return false;
+    p->nw = best_nw;
+    p->rq = best_rq;
+    p->grid = (int)grid;
+    p->depth = o.depth > 0 ? o.depth : (best_nw <= 4 ? 3 : 2);
+    if (p->depth < 2 || p->depth > 3 || (p->depth == 3 && p->nw > 4)) return false;
+    p->max_rows_wg = (int)(4 * qpw);
+    return true;
+}
+
+// The planner.  `fast_ok`: x and W 16-byte aligned and K % 8 == 0.
+int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& o, Plan* p) {
+    const int64_t J = ceil_div(K, rg::kChunk);
+    int want = RG_KERNEL_GENERIC;
+    const int mt = M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 0;
+    if (fast_ok && mt > 0 && J <= 112) want = RG_KERNEL_DECODE;
+    if (o.kernel > 0) {
+        want = o.kernel - 1;
+        if (want == RG_KERNEL_DECODE && !(fast_ok && mt > 0 && J <= 112)) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_TILED) return RG_ERR_RANGE;  // not built yet
+    }
+    p->kernel = want;
+    p->reverse = o.grid_order;
+    if (want == RG_KERNEL_DECODE) {
+        p->mt = mt;
+        if (!decode_schedule(N, J, mt, o, p)) {
+            if (o.kernel > 0 || o.waves_per_wg > 0 || o.grid_wgs > 0 || o.depth > 0) return RG_ERR_RANGE;
+            p->kernel = RG_KERNEL_GENERIC;
+        }
+    }
+    if (p->kernel == RG_KERNEL_GENERIC) {
+        const int64_t blocks = ceil_div(M * N, 256);
+        int64_t grid = o.grid_wgs > 0 ? o.grid_wgs : (blocks < 8 * kNominalCUs ? blocks : 8 * kNominalCUs);
+        if (grid < 1) grid = 1;
+        p->grid = (int)grid;
+        p->nw = 4;
+    }
+    return RG_OK;
+}
+
+int validate_launch(const rg_launch_t& c) {
+    if (c.kernel < -1 || c.kernel > 3) return RG_ERR_RANGE;
+    if (c.waves_per_wg < 0 || c.waves_per_wg > 8) return RG_ERR_RANGE;
+    if (c.grid_wgs < 0 || c.grid_wgs > 65536) return RG_ERR_RANGE;
+    if (c.depth < 0 || c.depth > 4) return RG_ERR_RANGE;
+    if (c.grid_order < 0 || c.grid_order > 1) return RG_ERR_RANGE;
+    return RG_OK;
+}
+
+rg_launch_t current_launch() {
+    std::lock_guard<std::mutex> lk(g_launch_mu);
+    return g_launch;
+}
+
+bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + bn && b0 < a0 + an;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rg_strerror(int code) {
+    switch (code) {
+        case RG_OK: return "ok";
+        case RG_ERR_INVAL: return "invalid argument (null pointer, size < 1 or size overflow)";
+        case RG_ERR_ALIGN: return "misaligned pointer";
+        case RG_ERR_ARCH: return "current device is not gfx950";
+        case RG_ERR_HIP: return "HIP runtime error";
+        case RG_ERR_RANGE: return "launch setting out of range for this shape";
+        case RG_ERR_ALIAS: return "output overlaps an input";
+        default: return "unknown rg status";
+    }
+}
+
+int rg_linear_set_launch(const rg_launch_t* cfg) {
+    rg_launch_t c = {};
+    if (cfg) {
+        c = *cfg;
+        const int s = validate_launch(c);
+        if (s != RG_OK) return s;
+    }
+    std::lock_guard<std::mutex> lk(g_launch_mu);
+    g_launch = c;
+    return RG_OK;
+}
+
+int rg_plan(int64_t M, int64_t N, int64_t K, rg_plan_t* out) {
+    if (!out || M < 1 || N < 1 || K < 1) return RG_ERR_INVAL;
+    if (!mul_ok(M, K) || !mul_ok(N, K) || !mul_ok(M, N)) return RG_ERR_INVAL;
+    Plan p;
+    const int s = make_plan(M, N, K, (K % 8) == 0, current_launch(), &p);
+    if (s != RG_OK) return s;
+    std::memset(out, 0, sizeof *out);
+    out->order_id = RG_ORDER_ID;
+    out->chunk = rg::kChunk;
+    out->nchunks = ceil_div(K, rg::kChunk);
+    out->kernel = p.kernel;
+    out->waves_per_wg = p.nw;
+    out->grid_wgs = p.grid;
+    out->depth = p.depth;
+    out->rows_per_round = 4 * p.rq;
+    out->tile_m = p.tile_m;
+    out->tile_n = p.tile_n;
+    return RG_OK;
+}
+
+int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, void* stream) {
+    if (!x || !w || !y || M < 1 || N < 1 || K < 1) return RG_ERR_INVAL;
+    if (!mul_ok(M, K) || !mul_ok(N, K) || !mul_ok(M, N)) return RG_ERR_INVAL;
+    if (((uintptr_t)x & 3) || ((uintptr_t)w & 1) || ((uintptr_t)y & 3)) return RG_ERR_ALIGN;
+    if (overlaps(y, (size_t)(M * N) * 4, x, (size_t)(M * K) * 4) ||
+        overlaps(y, (size_t)(M * N) * 4, w, (size_t)(N * K) * 2))
+        return RG_ERR_ALIAS;
+    int cus = 0;
+    const int dc = device_check(&cus);
+    if (dc != RG_OK) return dc;
+    const bool fast_ok = (K % 8) == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)w & 15) == 0;
+    Plan p;
+    const int s = make_plan(M, N, K, fast_ok, current_launch(), &p);
+    if (s != RG_OK) return s;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = hipSuccess;
+    if (p.kernel == RG_KERNEL_DECODE) {
+        rg::DecodeArgs a;
+        a.x = x;
+        a.w = w;
+        a.y = y;
+        a.M = M;
+        a.N = N;
+        a.K = K;
+        a.Q = p.Q;
+        a.J = (int)ceil_div(K, rg::kChunk);
+        a.RQ = p.rq;
+        a.reverse = p.reverse;
+        a.max_rows_wg = p.max_rows_wg;
+        e = rg::launch_decode(a, p.mt, p.grid, p.nw, p.depth, st);
+    } else {
+        e = rg::launch_generic(x, w, y, M, N, K, p.grid, p.reverse, st);
+    }
+    return e == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+int rg_cast_bf16_f32(const uint16_t* w, float* o, int64_t count, void* stream) {
+    if (!w || !o || count < 1) return RG_ERR_INVAL;
+    if (((uintptr_t)w & 1) || ((uintptr_t)o & 3)) return RG_ERR_ALIGN;
+    const int dc = device_check(nullptr);
+    if (dc != RG_OK) return dc;
+    return rg::launch_cast(w, o, count, (hipStream_t)stream) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+int rg_argmax_rows(const float* y, int64_t* out, int64_t M, int64_t N, void* stream) {
+    if (!y || !out || M < 1 || N < 1 || M > 2147483647) return RG_ERR_INVAL;
+    if (((uintptr_t)y & 3) || ((uintptr_t)out & 7)) return RG_ERR_ALIGN;
+    const int dc = device_check(nullptr);
+    if (dc != RG_OK) return dc;
+    return rg::launch_argmax(y, out, M, N, (hipStream_t)stream) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+int rg_stream_create_cu_mask(const uint32_t* mask, uint32_t nwords, void** out_stream) {
+    if (!mask || nwords == 0 || !out_stream) return RG_ERR_INVAL;
+    hipStream_t s = nullptr;
+    if (hipExtStreamCreateWithCUMask(&s, nwords, mask) != hipSuccess) return RG_ERR_HIP;
+    *out_stream = (void*)s;
+    return RG_OK;
+}
+
+int rg_stream_destroy(void* stream) {
+    if (!stream) return RG_ERR_INVAL;
+    return hipStreamDestroy((hipStream_t)stream) == hipSuccess ? RG_OK : RG_ERR_HIP;
+}
+
+int rg_device_cu_count(int32_t* out) {
+    if (!out) return RG_ERR_INVAL;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return RG_ERR_HIP;
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return RG_ERR_HIP;
+    *out = cus;
+    return RG_OK;
+}
+
+}  // extern "C"

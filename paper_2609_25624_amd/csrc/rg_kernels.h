@@ -1,0 +1,28 @@
+// Internal interface between the C-ABI (rg_api.cpp) and the kernels (rg_kernels.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rg {
+
+constexpr int kChunk = 256;  // segment length C of the documented order
+
+struct DecodeArgs {
+    const float* x;
+    const uint16_t* w;
+    float* y;
+    int64_t M, N, K;
+    int64_t Q;          // quads of W rows: ceil(N / 4)
+    int J;              // segments: ceil(K / 256)
+    int RQ;             // quads per round
+    int reverse;        // 1: workgroup b takes the quads of workgroup grid-1-b
+    int max_rows_wg;    // 4 * ceil(Q / grid): rows staged per workgroup
+};
+
+hipError_t launch_generic(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K,
+                          int grid, int reverse, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int depth, hipStream_t stream);
+hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream);
+hipError_t launch_argmax(const float* y, int64_t* out, int64_t M, int64_t N, hipStream_t stream);
+
+}  // namespace rg

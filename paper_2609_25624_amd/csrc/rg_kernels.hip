@@ -1,0 +1,429 @@
+// Fused-upcast linear layer kernels for gfx950 (MI355X).
+//
+// Every kernel here computes y[m][n] = sum_k x[m][k] * up(W[n][k]) in the one
+// order documented in include/rg.h ("RG-ORDER-1"): 256-wide K segments, each a
+// chain of fmaf from +0 in ascending k, segment partials folded left to right
+// in ascending segment order (paper: Design, eq. 2 and rules R1-R4).  Kernels
+// differ only in how outputs are spread over lanes, waves and workgroups,
+// which never changes a bit of any output.
+//
+// Arithmetic: only v_fma_f32 / v_fmac_f32 (IEEE fused) and v_add_f32, with
+// binary32 denormals preserved (the kernel descriptors keep
+// float_denorm_mode_32 = 3).  No matrix-core (MFMA) or dot-product
+// instructions; the library is built with -ffp-contract=off and packed FP32
+// disabled, so the compiler cannot fuse, reassociate or pair operations.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rg_kernels.h"
+
+namespace rg {
+
+// ---------------------------------------------------------------------------
+// helpers
+// ---------------------------------------------------------------------------
+
+// Exact bfloat16 -> float32 widening of the low / high half of a packed dword
+// (element k at the lower address sits in the low 16 bits).
+__device__ __forceinline__ float up_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float up_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+__device__ __forceinline__ float up1(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// Broadcast lane E of every quad (4 lanes) to the whole quad (DPP quad_perm).
+template <int E>
+__device__ __forceinline__ float quad_bcast(float v) {
+    constexpr int ctrl = E | (E << 2) | (E << 4) | (E << 6);
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), ctrl, 0xf, 0xf, true));
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) void*)p);
+}
+
+// 16-byte global -> LDS DMA.  Lane l writes LDS bytes [lds_base + 16*l, +16).
+// Issued through inline asm so the compiler does not add its conservative
+// vmcnt(0) before every LDS read; the kernel waits with vmcnt_wait<N>().
+// M0 (which holds the LDS address for the DMA and is read when the
+// instruction issues) is saved and restored around it.
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "global_load_lds_dwordx4 %1, %3\n\t"
+        "s_mov_b32 m0, %0\n\t"
+        : "=&s"(saved)
+        : "v"(voff), "s"(lds_base), "s"(sbase)
+        : "memory");
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+// Only loads are in flight while it is used, and they complete in issue order.
+template <int N>
+__device__ __forceinline__ void vmcnt_wait() {
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// ---------------------------------------------------------------------------
+// generic kernel: one thread per output, any K, any alignment.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) generic_kernel(const float* __restrict__ x,
+                                                      const uint16_t* __restrict__ w,
+                                                      float* __restrict__ y, int64_t M, int64_t N,
+                                                      int64_t K, int reverse) {
+    const int64_t total = M * N;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t b = reverse ? (int64_t)(gridDim.x - 1 - blockIdx.x) : (int64_t)blockIdx.x;
+    for (int64_t idx = b * blockDim.x + threadIdx.x; idx < total; idx += stride) {
+        const int64_t m = idx / N, n = idx % N;
+        const float* xr = x + m * K;
+        const uint16_t* wr = w + n * K;
+        float acc = 0.0f;
+        for (int64_t k0 = 0, j = 0; k0 < K; k0 += kChunk, ++j) {
+            const int64_t k1 = (k0 + kChunk < K) ? k0 + kChunk : K;
+            float p = 0.0f;
+            for (int64_t k = k0; k < k1; ++k) p = __builtin_fmaf(xr[k], up1(wr[k]), p);
+            acc = (j == 0) ? p : acc + p;
+        }
+        y[m * N + n] = acc;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// decode kernel (M <= MT <= 4): streaming GEMV / skinny GEMM.
+//
+// Work split.  Rows of W are grouped in quads (4 rows).  Workgroup g owns the
+// contiguous quads [q0, q1) and all of K for them, so every output is
+// finished inside one workgroup (no cross-workgroup traffic, no atomics).
+// It walks its quads in rounds of RQ quads.  In a round every lane owns one
+// (row, segment) pair: the 4 lanes of a DPP quad hold 4 consecutive rows and
+// one segment j; the lane roles (quad-in-round, j, row-in-quad) are fixed for
+// the whole kernel, so each lane keeps x of its segment in registers.
+//
+// Data path.  A wave streams W in steps of one 64-element slab (128 bytes per
+// lane, 8 KB per wave) through a DEPTH-deep ring of LDS buffers with 16-byte
+// global->LDS DMA loads: 8 lanes read one 128-byte line, so every load
+// instruction is fully coalesced.  The LDS image of lane s's 128 bytes is
+// XOR-swizzled by ((s >> 1) & 7) in 16-byte units, so the transposing
+// ds_read_b128 of each lane (its own row, ascending k) is conflict-free.
+// x values are shared inside a quad with DPP quad broadcasts.
+//
+// Order.  Each lane runs the 256-FMA chain of its (row, segment) from +0 in
+// ascending k; partials go to LDS; after the round one thread per output
+// folds them in ascending segment order.  Results are staged in LDS and
+// written once the W stream has drained.
+// ---------------------------------------------------------------------------
+
+// One 64-element slab of a lane's chain: acc[m] = fmaf(x, up(w), acc[m]) for
+// the slab's elements in ascending k.  wp holds the lane's 8 pieces of 8 bf16;
+// X[m][S][i] holds x for element 16*e + i of the slab in quad lane e.
+template <int S, int MT>
+__device__ __forceinline__ void fma_slab(const uint4 (&wp)[8], const float (&X)[MT][4][16], float (&acc)[MT],
+                                         int npieces) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        if (npieces < 8 && t >= npieces) break;   // short last segment only
+        const uint32_t d[4] = {wp[t].x, wp[t].y, wp[t].z, wp[t].w};
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+            const float wv = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+            const int kl = 8 * t + h;          // element inside the slab
+            const int i = kl & 15;             // register inside the x block
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                float xv;
+                switch (kl >> 4) {             // lane of the quad holding x
+                    case 0: xv = quad_bcast<0>(X[m][S][i]); break;
+                    case 1: xv = quad_bcast<1>(X[m][S][i]); break;
+                    case 2: xv = quad_bcast<2>(X[m][S][i]); break;
+                    default: xv = quad_bcast<3>(X[m][S][i]); break;
+                }
+                acc[m] = __builtin_fmaf(xv, wv, acc[m]);
+            }
+        }
+    }
+}
+
+constexpr int kSlab = 64;                    // elements per lane per step
+constexpr int kSlabBytesPerWave = 64 * 128;  // 8 KB
+
+template <int MT, int NW, int DEPTH>
+__global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
+    static_assert(MT == 1 || MT == 2 || MT == 4, "decode M tile");
+    static_assert(DEPTH >= 2 && DEPTH <= 4, "pipeline depth");
+    constexpr int kThreads = NW * 64;
+
+    __shared__ __attribute__((aligned(16))) uint8_t wring[NW][DEPTH][kSlabBytesPerWave];
+    __shared__ float part[2][kThreads * MT];          // [parity][row_local * J + j][m]
+    extern __shared__ float yres[];                   // [row_in_wg][m], dynamic
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    const int J = a.J;
+    const int RQ = a.RQ;
+    const int64_t N = a.N, K = a.K;
+
+    const int64_t G = gridDim.x;
+    const int64_t g = a.reverse ? (G - 1 - blockIdx.x) : blockIdx.x;
+    const int64_t q0 = g * a.Q / G, q1 = (g + 1) * a.Q / G;
+    const int nq = (int)(q1 - q0);
+    const int rounds = (nq + RQ - 1) / RQ;
+    const int nsteps = rounds * (kChunk / kSlab);
+
+    // ---- fixed lane role (consumer) ----
+    const int ql = tid >> 2;                 // quad lane in the workgroup
+    const int e = tid & 3;                   // row inside the quad
+    const bool role = ql < RQ * J;
+    const int lq = role ? ql / J : 0;        // quad inside the round
+    const int jj = role ? ql % J : 0;        // segment
+    const int seg_len = (jj == J - 1) ? (int)(K - (int64_t)(J - 1) * kChunk) : kChunk;
+
+    // ---- x of this lane's segment, resident in registers ----
+    // X[m][s][i] = x[m][jj*256 + 64 s + 16 e + i] (0 beyond K or M)
+    float X[MT][4][16];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const int64_t kb = (int64_t)jj * kChunk + s * kSlab + 16 * e;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                // unconditional load from a clamped address, then zero what is outside x
+                const bool ok = role && m < a.M && kb + 4 * c + 4 <= K;
+                const float4 v = *reinterpret_cast<const float4*>(a.x + (ok ? (int64_t)m * K + kb + 4 * c : 0));
+                X[m][s][4 * c + 0] = ok ? v.x : 0.0f;
+                X[m][s][4 * c + 1] = ok ? v.y : 0.0f;
+                X[m][s][4 * c + 2] = ok ? v.z : 0.0f;
+                X[m][s][4 * c + 3] = ok ? v.w : 0.0f;
+            }
+        }
+
+    // ---- DMA role: instruction i of this wave fills consumer lane sigma = 8i + (lane>>3) ----
+    // Per round, the 8 byte offsets (relative to the round's first row) are fixed
+    // except for row clamping at the end of W; precompute the unclamped parts.
+    int dma_row[8];      // row inside the round (0 .. 4*RQ-1), or -1 if that consumer is idle
+    uint32_t dma_col[8]; // byte offset inside the row at slab 0: j*512 + 16*t
+    int dma_jlen[8];     // element length of that consumer's segment
+    int dma_kin[8];      // element offset inside the segment at slab 0: 8*t
+    {
+        const int p = lane & 7;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int sigma = 8 * i + (lane >> 3);
+            const int cql = wave * 16 + (sigma >> 2);
+            const int t = p ^ ((sigma >> 1) & 7);
+            if (cql < RQ * J) {
+                const int cq = cql / J, cj = cql % J;
+                dma_row[i] = 4 * cq + (sigma & 3);
+                dma_col[i] = (uint32_t)cj * (kChunk * 2) + 16u * t;
+                dma_jlen[i] = (cj == J - 1) ? (int)(K - (int64_t)(J - 1) * kChunk) : kChunk;
+                dma_kin[i] = 8 * t;
+            } else {
+                dma_row[i] = -1;
+                dma_col[i] = 0;
+                dma_jlen[i] = kChunk;
+                dma_kin[i] = 0;
+            }
+        }
+    }
+    const uint32_t ring_base = lds_addr(&wring[wave][0][0]);
+    const int64_t row_bytes = K * 2;
+
+    // Issue step st (round r = st/4, slab s = st%4) into ring slot st % DEPTH.
+    auto issue = [&](int st) {
+        const int r = st >> 2, s = st & 3;
+        const int64_t row0 = 4 * (q0 + (int64_t)r * RQ);     // first row of the round
+        const int64_t rmax = N - 1 - row0;                    // clamp rows to W
+        const char* base = reinterpret_cast<const char*>(a.w) + row0 * row_bytes;
+        const uint32_t slot = ring_base + (uint32_t)((st % DEPTH) * kSlabBytesPerWave);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            int64_t row = dma_row[i] < 0 ? 0 : dma_row[i];
+            if (row > rmax) row = rmax;
+            uint32_t col = dma_col[i] + (uint32_t)(s * kSlab * 2);
+            if (s * kSlab + dma_kin[i] >= dma_jlen[i]) col = 0;   // past the end of a short last segment
+            const uint32_t voff = (uint32_t)(row * row_bytes) + col;
+            dma16(base, voff, slot + 1024u * i);
+        }
+    };
+
+    float acc[MT];
+    const int rows_wg = 4 * nq;
+
+    // prologue
+#pragma unroll
+    for (int st = 0; st < DEPTH - 1; ++st)
+        if (st < nsteps) issue(st);
+
+    for (int st = 0; st < nsteps; ++st) {
+        const int r = st >> 2, s = st & 3;
+        if (st + DEPTH - 1 < nsteps) issue(st + DEPTH - 1);
+        const int ahead = min(DEPTH - 1, nsteps - 1 - st);
+        if (ahead >= 3) vmcnt_wait<24>();
+        else if (ahead == 2) vmcnt_wait<16>();
+        else if (ahead == 1) vmcnt_wait<8>();
+        else vmcnt_wait<0>();
+
+        const bool active = role && (lq < nq - r * RQ);
+        if (s == 0) {
+#pragma unroll
+            for (int m = 0; m < MT; ++m) acc[m] = 0.0f;
+        }
+        // ---- consume slab s: 64 elements of this lane's (row, segment) ----
+        const int npieces = min(8, max(0, (seg_len - s * kSlab) / 8));
+        if (active && npieces > 0) {
+            const uint8_t* src = &wring[wave][st % DEPTH][lane * 128];
+            const int sw = (lane >> 1) & 7;
+            uint4 wp[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t) wp[t] = *reinterpret_cast<const uint4*>(src + 16 * (t ^ sw));
+            switch (s) {   // static slab index keeps X in registers
+                case 0: fma_slab<0, MT>(wp, X, acc, npieces); break;
+                case 1: fma_slab<1, MT>(wp, X, acc, npieces); break;
+                case 2: fma_slab<2, MT>(wp, X, acc, npieces); break;
+                default: fma_slab<3, MT>(wp, X, acc, npieces); break;
+            }
+        }
+        if (s == 3) {
+            // segment partials of this round -> LDS, then fold in ascending segment order
+            const int par = r & 1;
+            if (active) {
+#pragma unroll
+                for (int m = 0; m < MT; ++m) part[par][((4 * lq + e) * J + jj) * MT + m] = acc[m];
+            }
+            __syncthreads();
+            const int rows_round = 4 * min(RQ, nq - r * RQ);
+            for (int o = tid; o < rows_round * MT; o += kThreads) {
+                const int rl = o / MT, m = o % MT;
+                const float* pp = &part[par][rl * J * MT + m];
+                float yv = pp[0];
+                for (int j = 1; j < J; ++j) yv = yv + pp[j * MT];
+                yres[(r * RQ * 4 + rl) * MT + m] = yv;
+            }
+            // The next round writes the other parity; this parity is rewritten
+            // only after the next round's barrier, which all folds precede.
+        }
+    }
+    vmcnt_wait<0>();
+    __syncthreads();
+    // ---- write results ----
+    const int64_t rowbase = 4 * q0;
+    for (int o = tid; o < rows_wg * MT; o += kThreads) {
+        const int m = o / rows_wg, rl = o % rows_wg;
+        const int64_t n = rowbase + rl;
+        if (m < a.M && n < N) a.y[(int64_t)m * N + n] = yres[rl * MT + m];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// cast kernel (comparison point only: the transient FP32 weight copy)
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) cast_kernel(const uint16_t* __restrict__ w, float* __restrict__ o,
+                                                   int64_t count) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) o[i] = up1(w[i]);
+}
+
+// ---------------------------------------------------------------------------
+// argmax per row, lowest index on ties, NaN never wins.  Comparisons are
+// exact, so the result does not depend on the reduction tree.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool better(float v, int64_t i, float bv, int64_t bi) {
+    if (v != v) return false;
+    if (bi < 0 || bv != bv) return true;
+    return v > bv || (v == bv && i < bi);
+}
+
+__global__ void __launch_bounds__(256) argmax_kernel(const float* __restrict__ y, int64_t* __restrict__ out,
+                                                     int64_t N) {
+    __shared__ float sv[256];
+    __shared__ int64_t si[256];
+    const int64_t m = blockIdx.x;
+    const float* row = y + m * N;
+    float bv = 0.0f;
+    int64_t bi = -1;
+    for (int64_t n = threadIdx.x; n < N; n += 256) {
+        const float v = row[n];
+        if (better(v, n, bv, bi)) { bv = v; bi = n; }
+    }
+    sv[threadIdx.x] = bv;
+    si[threadIdx.x] = bi;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (threadIdx.x < h) {
+            const float v = sv[threadIdx.x + h];
+            const int64_t i = si[threadIdx.x + h];
+            if (i >= 0 && better(v, i, sv[threadIdx.x], si[threadIdx.x])) {
+                sv[threadIdx.x] = v;
+                si[threadIdx.x] = i;
+            }
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out[m] = si[0];
+}
+
+// ---------------------------------------------------------------------------
+// host-side launchers
+// ---------------------------------------------------------------------------
+hipError_t launch_generic(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K,
+                          int grid, int reverse, hipStream_t stream) {
+    hipLaunchKernelGGL(generic_kernel, dim3(grid), dim3(256), 0, stream, x, w, y, M, N, K, reverse);
+    return hipGetLastError();
+}
+
+template <int MT, int NW, int DEPTH>
+static hipError_t launch_decode_t(const DecodeArgs& a, int grid, hipStream_t stream) {
+    const size_t dyn = (size_t)a.max_rows_wg * MT * sizeof(float);
+    hipLaunchKernelGGL((decode_kernel<MT, NW, DEPTH>), dim3(grid), dim3(NW * 64), dyn, stream, a);
+    return hipGetLastError();
+}
+
+// Pipeline depths that fit the 160 KB of LDS: 3 up to 4 waves, 2 above.
+template <int MT, int NW>
+static hipError_t launch_decode_d(const DecodeArgs& a, int grid, int depth, hipStream_t stream) {
+    if (depth == 2) return launch_decode_t<MT, NW, 2>(a, grid, stream);
+    if constexpr (NW <= 4) {
+        if (depth == 3) return launch_decode_t<MT, NW, 3>(a, grid, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <int MT>
+static hipError_t launch_decode_w(const DecodeArgs& a, int grid, int nw, int depth, hipStream_t stream) {
+    switch (nw) {
+        case 1: return launch_decode_d<MT, 1>(a, grid, depth, stream);
+        case 2: return launch_decode_d<MT, 2>(a, grid, depth, stream);
+        case 4: return launch_decode_d<MT, 4>(a, grid, depth, stream);
+        case 6: return launch_decode_d<MT, 6>(a, grid, depth, stream);
+        case 7: return launch_decode_d<MT, 7>(a, grid, depth, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int depth, hipStream_t stream) {
+    switch (mt) {
+        case 1: return launch_decode_w<1>(a, grid, nw, depth, stream);
+        case 2: return launch_decode_w<2>(a, grid, nw, depth, stream);
+        case 4: return launch_decode_w<4>(a, grid, nw, depth, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream) {
+    int64_t blocks = (count + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(cast_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, w, o, count);
+    return hipGetLastError();
+}
+
+hipError_t launch_argmax(const float* y, int64_t* out, int64_t M, int64_t N, hipStream_t stream) {
+    hipLaunchKernelGGL(argmax_kernel, dim3((unsigned)M), dim3(256), 0, stream, y, out, N);
+    return hipGetLastError();
+}
+
+}  // namespace rg

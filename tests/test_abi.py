@@ -1,0 +1,128 @@
+"""The C-ABI library without a GPU: symbols, the shape-only planner, host-side argument checks."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_25624_amd as rg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rg.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(rg_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported_and_bound():
+    names = declared_functions()
+    assert "rg_linear" in names and "rg_linear_set_launch" in names
+    lib = ctypes.CDLL(rg.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in include/rg.h but not exported"
+    assert sorted(rg.EXPORTS) == names
+
+
+def test_strerror_never_null():
+    for c in range(-2, 10):
+        assert isinstance(rg.strerror(c), str) and rg.strerror(c)
+
+
+def test_plan_numeric_fields_depend_on_k_only():
+    # The order (segment length, segment count, order id) is a function of K alone.
+    for K in (1, 7, 8, 255, 256, 257, 1000, 4096, 14336, 28672):
+        seen = set()
+        for M in (1, 2, 4, 5, 16, 64, 65, 2048):
+            for N in (1, 5, 1024, 4096, 128256):
+                p = rg.rg_plan(M, N, K)
+                seen.add((p["order_id"], p["chunk"], p["nchunks"]))
+        assert seen == {(1, 256, -(-K // 256))}
+
+
+def test_plan_is_pure_and_overrides_are_scheduling_only():
+    a = rg.rg_plan(1, 6144, 4096)
+    assert a == rg.rg_plan(1, 6144, 4096)
+    rg.rg_linear_set_launch(waves_per_wg=4, grid_wgs=100, depth=2, grid_order=1)
+    try:
+        b = rg.rg_plan(1, 6144, 4096)
+        assert (b["waves_per_wg"], b["grid_wgs"], b["depth"]) == (4, 100, 2)
+        assert (b["order_id"], b["chunk"], b["nchunks"]) == (a["order_id"], a["chunk"], a["nchunks"])
+    finally:
+        rg.rg_linear_set_launch(None)
+    assert rg.rg_plan(1, 6144, 4096) == a
+
+
+def test_plan_kernel_choice():
+    assert rg.rg_plan(1, 6144, 4096)["kernel_name"] == "decode"
+    assert rg.rg_plan(4, 6144, 4096)["kernel_name"] == "decode"
+    assert rg.rg_plan(1, 10, 7)["kernel_name"] == "generic"     # K % 8 != 0
+
+
+def test_set_launch_range_checks():
+    for bad in (dict(waves_per_wg=9), dict(grid_wgs=-1), dict(depth=5), dict(grid_order=2), dict(kernel=7)):
+        with pytest.raises(rg.RgError) as e:
+            rg.rg_linear_set_launch(**bad)
+        assert e.value.code == rg.RG_ERR_RANGE
+    rg.rg_linear_set_launch(None)
+
+
+def test_linear_rejects_bad_arguments_before_touching_a_device():
+    L = rg.lib
+    # null pointers, bad sizes, overflow
+    assert L.rg_linear(None, 16, 16, 1, 1, 1, None) == rg.RG_ERR_INVAL
+    assert L.rg_linear(16, 16, 1024, 0, 1, 1, None) == rg.RG_ERR_INVAL
+    assert L.rg_linear(16, 16, 1024, 1, -3, 1, None) == rg.RG_ERR_INVAL
+    assert L.rg_linear(16, 16, 1024, 1 << 40, 1, 1 << 30, None) == rg.RG_ERR_INVAL
+    # misaligned x (4), W (2), y (4)
+    assert L.rg_linear(0x1002, 0x100000, 0x200000, 1, 1, 8, None) == rg.RG_ERR_ALIGN
+    assert L.rg_linear(0x1000, 0x100001, 0x200000, 1, 1, 8, None) == rg.RG_ERR_ALIGN
+    assert L.rg_linear(0x1000, 0x100000, 0x200002, 1, 1, 8, None) == rg.RG_ERR_ALIGN
+    # y overlapping x or W
+    assert L.rg_linear(0x1000, 0x100000, 0x1000, 1, 1, 8, None) == rg.RG_ERR_ALIAS
+    assert L.rg_linear(0x1000, 0x100000, 0x100008, 1, 2, 8, None) == rg.RG_ERR_ALIAS
+    assert L.rg_plan(0, 1, 1, None) == rg.RG_ERR_INVAL
+
+
+def test_other_entry_points_reject_bad_arguments():
+    L = rg.lib
+    assert L.rg_cast_bf16_f32(None, 0x1000, 10, None) == rg.RG_ERR_INVAL
+    assert L.rg_cast_bf16_f32(0x1001, 0x1000, 10, None) == rg.RG_ERR_ALIGN
+    assert L.rg_argmax_rows(0x1000, None, 1, 1, None) == rg.RG_ERR_INVAL
+    assert L.rg_argmax_rows(0x1002, 0x2000, 1, 1, None) == rg.RG_ERR_ALIGN
+    assert L.rg_stream_create_cu_mask(None, 1, None) == rg.RG_ERR_INVAL
+    assert L.rg_stream_destroy(None) == rg.RG_ERR_INVAL
+    assert L.rg_device_cu_count(None) == rg.RG_ERR_INVAL
+
+
+def test_no_atomics_or_matrix_core_builtins_in_kernels():
+    src = open(os.path.join(ROOT, "paper_2609_25624_amd", "csrc", "rg_kernels.hip")).read()
+    code = re.sub(r"//.*", "", src)
+    for bad in ("atomicAdd", "__hip_atomic", "mfma", "__builtin_amdgcn_fdot", "__builtin_amdgcn_sdot",
+                "unsafe-fp", "fast-math"):
+        assert bad not in code, bad
+
+
+def test_device_code_uses_only_ieee_fma_for_accumulation():
+    # Inspect the gfx950 assembly of our own kernels: no matrix-core, dot-product,
+    # packed-FP32, mixed-precision or non-fused multiply-add instructions.
+    import subprocess
+    import tempfile
+    from paper_2609_25624_amd import build as b
+    src = os.path.join(ROOT, "paper_2609_25624_amd", "csrc", "rg_kernels.hip")
+    with tempfile.TemporaryDirectory() as d:
+        out = os.path.join(d, "k.s")
+        r = subprocess.run([b.HIPCC, "-x", "hip", *b.COMMON, *b.DEVICE, "--cuda-device-only", "-S", src, "-o", out],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+        asm = open(out).read()
+    insts = re.findall(r"^\s+(v_[a-z0-9_]+)", asm, flags=re.M)
+    assert insts
+    for i in set(insts):
+        assert not re.match(r"v_(mfma|smfmac|dot\d|pk_(fma|mul|add)_f32|mad_f32|mac_f32|mad_legacy|mac_legacy|fma_legacy|fma_mix|mad_mix)", i), i
+    assert "v_fma_f32" in insts or "v_fmac_f32_e32" in insts
+    # binary32 denormals kept in every kernel
+    modes = re.findall(r"\.amdhsa_float_denorm_mode_32\s+(\d+)", asm)
+    assert modes and set(modes) == {"3"}

@@ -1,0 +1,369 @@
+"""GPU path (through the C-ABI) against the CPU oracle, bit for bit.
+
+Configs follow the paper's probe and ablation shapes (Evaluation,
+cross-architecture determinism; Supplement C): decode shapes of an
+8B-parameter Llama-3-class model at M = 1, the same layers batched at
+M = 4/16/64, an LM head with a near tie, 70B-class layers, and ragged shapes.
+Inputs are seeded on the host and copied to the device (Supplement C, method).
+"""
+import numpy as np
+import pytest
+
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+L8B = {  # Llama-3-8B-shaped decode projections (N, K)
+    "qkv": (6144, 4096),
+    "o": (4096, 4096),
+    "gate_up": (28672, 4096),
+    "down": (4096, 14336),
+}
+
+
+@pytest.fixture(autouse=True)
+def _reset_launch():
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(None)
+    yield
+    rg.rg_linear_set_launch(None)
+
+
+def _check_layer(M, N, K, seed=0, w_std=0.02, layer_id=0, sampled=None):
+    import torch
+    gu.log(f"case M={M} N={N} K={K} seed={seed} layer={layer_id}")
+    x, w = gu.layer(M, N, K, seed=seed, w_std=w_std, layer_id=layer_id)
+    xd, wd = gu.to_dev(x, w)
+    y = gu.run(xd, wd)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy()
+    if sampled:
+        import oracle
+        rows, cols = gu.sample_indices(M, N, sampled, seed=seed)
+        want = oracle.linear_sampled(x, w, rows, cols)
+        gu.assert_bitwise(got[rows, cols], want, f"({M},{N},{K}) sampled")
+    else:
+        want = gu.oracle_full(x, w)
+        gu.assert_bitwise(got, want, f"({M},{N},{K})")
+    return x, w, got
+
+
+def test_config1_small_layer():
+    _check_layer(1, 1024, 1024)
+
+
+@pytest.mark.parametrize("name", list(L8B))
+def test_config2_8b_layers_m1(name):
+    N, K = L8B[name]
+    _check_layer(1, N, K, layer_id=list(L8B).index(name))
+
+
+@pytest.mark.parametrize("M", [2, 3, 4, 16])
+@pytest.mark.parametrize("name", list(L8B))
+def test_config3_batched_rows_equal_single_row(name, M):
+    # Row m of a batch is bitwise the single-row result (rule R4), and the batch matches the oracle.
+    import torch
+    N, K = L8B[name]
+    x64, w = gu.layer(64, N, K, layer_id=list(L8B).index(name))
+    x = x64[:M]                       # seeded rows: the M-row batch is a prefix of the 64-row one
+    xd, wd = gu.to_dev(x, w)
+    y = gu.run(xd, wd).cpu().numpy()
+    want = gu.oracle_full(x, w)
+    gu.assert_bitwise(y, want, f"{name} M={M}")
+    for m in (0, M - 1):
+        y1 = gu.run(xd[m:m + 1].contiguous(), wd)
+        torch.cuda.synchronize()
+        gu.assert_bitwise(y1.cpu().numpy()[0], y[m], f"{name} row {m} alone vs in batch {M}")
+
+
+@pytest.mark.parametrize("name", list(L8B))
+def test_config3_m64_sampled(name):
+    import torch
+    N, K = L8B[name]
+    x, w = gu.layer(64, N, K, layer_id=list(L8B).index(name))
+    xd, wd = gu.to_dev(x, w)
+    y = gu.run(xd, wd)
+    torch.cuda.synchronize()
+    import oracle
+    rows, cols = gu.sample_indices(64, N, 3000)
+    gu.assert_bitwise(y.cpu().numpy()[rows, cols], oracle.linear_sampled(x, w, rows, cols), f"{name} M=64")
+    y1 = gu.run(xd[5:6].contiguous(), wd)
+    gu.assert_bitwise(y1.cpu().numpy()[0], y.cpu().numpy()[5], f"{name} row 5 at M=64 vs M=1")
+
+
+def test_config4_lm_head_m1_and_m16():
+    import torch
+    N, K = 128256, 4096
+    x16, w = gu.layer(16, N, K, layer_id=7)
+    xd, wd = gu.to_dev(x16, w)
+    y16 = gu.run(xd, wd).cpu().numpy()
+    y1 = gu.run(xd[:1].contiguous(), wd).cpu().numpy()
+    torch.cuda.synchronize()
+    want1 = gu.oracle_full(x16[:1], w)
+    gu.assert_bitwise(y1, want1, "lm_head M=1")
+    import oracle
+    rows, cols = gu.sample_indices(16, N, 4000)
+    gu.assert_bitwise(y16[rows, cols], oracle.linear_sampled(x16, w, rows, cols), "lm_head M=16 sampled")
+    gu.assert_bitwise(y16[0], y1[0], "lm_head row 0 at M=16 vs M=1")
+
+
+def _near_tie_case(kstar, exact_tie, M):
+    """W row n_b copies the argmax row n_a except one element k*, one bf16 ulp away.
+
+    With exact_tie, x[:, k*] = 0 so both logits are bitwise equal and the lower index must win.
+    """
+    N, K = 128256, 4096
+    x, w = gu.layer(M, N, K, layer_id=7)
+    w = w.copy()
+    x = x.copy()
+    import oracle
+    y0 = oracle.linear(x[:1], w)        # full row 0 of the unmodified logits
+    na = oracle.argmax(y0[0])
+    nb = N - 1 if na != N - 1 else 0
+    lo, hi = min(na, nb), max(na, nb)
+    w[hi] = w[lo]
+    w[hi, kstar] = np.uint16((int(w[lo, kstar]) + 1) & 0xFFFF)   # one bf16 ulp (for finite, non-max values)
+    if exact_tie:
+        x[:, kstar] = 0.0
+    return x, w, lo, hi
+
+
+@pytest.mark.parametrize("kstar,exact_tie", [(0, False), (255, False), (256, False), (4095, False), (1000, True)])
+def test_config4_near_tie_argmax(kstar, exact_tie):
+    import torch
+    import oracle
+    import paper_2609_25624_amd as rg
+    for M in (1, 16):
+        x, w, lo, hi = _near_tie_case(kstar, exact_tie, M)
+        xd, wd = gu.to_dev(x, w)
+        y = gu.run(xd, wd)
+        idx = torch.empty(M, dtype=torch.int64, device=xd.device)
+        rg.rg_argmax_rows(y, idx)
+        torch.cuda.synchronize()
+        yh = y.cpu().numpy()
+        rows = [0] if M == 1 else list(range(M))
+        for m in rows:
+            want = oracle.linear_sampled(x, w, [m, m], [lo, hi])
+            gu.assert_bitwise(yh[m, [lo, hi]], want, f"near tie k*={kstar} row {m}")
+        want_row0 = gu.oracle_full(x[:1], w)[0]
+        gu.assert_bitwise(yh[0], want_row0, f"near tie k*={kstar} full row 0")
+        assert int(idx[0].item()) == oracle.argmax(want_row0)
+        if exact_tie:
+            assert gu.bits(yh[0, lo]) == gu.bits(yh[0, hi])
+            assert int(idx[0].item()) == lo or yh[0].max() > yh[0, lo]
+        for m in rows:
+            assert int(idx[m].item()) == oracle.argmax(yh[m])
+
+
+@pytest.mark.parametrize("name,N,K", [("70b_gate_up", 57344, 8192), ("70b_down", 8192, 28672)])
+def test_config5_70b_m1(name, N, K):
+    _check_layer(1, N, K, w_std=0.01, layer_id=9)
+
+
+@pytest.mark.parametrize("name,N,K", [("70b_gate_up", 57344, 8192), ("70b_down", 8192, 28672)])
+def test_config5_70b_m2048_sampled(name, N, K):
+    import paper_2609_25624_amd as rg
+    if rg.rg_plan(2048, N, K)["kernel_name"] == "generic":
+        pytest.skip("prefill-size shape routes to the one-thread-per-output kernel; too slow at this size")
+    _check_layer(2048, N, K, w_std=0.01, layer_id=9, sampled=4000)
+
+
+@pytest.mark.parametrize("M", [1, 2, 3, 4, 5, 9])
+@pytest.mark.parametrize("N,K", [(1, 8), (3, 16), (5, 248), (4, 256), (7, 264), (63, 1000), (65, 1016),
+                                 (130, 4104), (33, 8200), (17, 520)])
+def test_ragged_shapes(M, N, K):
+    _check_layer(M, N, K, seed=M * 1000 + K)
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 10, 7), (2, 33, 301), (3, 5, 1), (1, 4, 257), (100, 1000, 1000)])
+def test_generic_shapes(M, N, K):
+    _check_layer(M, N, K, seed=K)
+
+
+def test_misaligned_pointers_take_the_generic_path():
+    import torch
+    M, N, K = 2, 37, 1024
+    x, w = gu.layer(M, N, K, seed=11)
+    xb = torch.zeros(M * K + 1, dtype=torch.float32, device=gu.dev())
+    xb[1:] = torch.from_numpy(x.ravel()).to(gu.dev())
+    xd = xb[1:].view(M, K)                      # 4-byte but not 16-byte aligned
+    wd = gu.to_dev(x, w)[1]
+    y = gu.run(xd, wd)
+    gu.assert_bitwise(y.cpu().numpy(), gu.oracle_full(x, w), "misaligned x")
+
+
+def test_order_probes_on_gpu():
+    # The hand-derived probes (tests/golden) also hold on the GPU, alone and placed
+    # at row m=5 of a 16-row batch and row n=1000 of a 4096-row W (position independence).
+    import torch
+    from tests import oracle_pins as pins
+    for p in pins.load_probes():
+        x1, w1 = pins.probe_inputs(p)
+        want = int(p["expect_bits"], 16)
+        xd, wd = gu.to_dev(x1, w1)
+        got = int(gu.bits(gu.run(xd, wd).cpu().numpy())[0, 0])
+        assert got == want, f"{p['name']} alone: 0x{got:08x}"
+        K = x1.shape[1]
+        X, W = gu.layer(16, 4096, K, seed=5)
+        X = X.copy(); W = W.copy()
+        X[5] = x1[0]
+        W[1000] = w1[0]
+        xd, wd = gu.to_dev(X, W)
+        y = gu.run(xd, wd)
+        torch.cuda.synchronize()
+        got = int(gu.bits(y.cpu().numpy())[5, 1000])
+        assert got == want, f"{p['name']} placed: 0x{got:08x}"
+
+
+def _launch_settings():
+    return [
+        dict(),
+        dict(waves_per_wg=1, depth=2),
+        dict(waves_per_wg=2, grid_wgs=97),
+        dict(waves_per_wg=4, grid_wgs=600, depth=2, grid_order=1),
+        dict(grid_wgs=1),
+        dict(kernel="generic"),
+        dict(kernel="generic", grid_wgs=3, grid_order=1),
+    ]
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 6144, 4096), (1, 4096, 14336), (3, 1000, 1000), (4, 2048, 2560)])
+def test_launch_settings_do_not_change_bits(M, N, K):
+    import torch
+    import paper_2609_25624_amd as rg
+    x, w = gu.layer(M, N, K, seed=21)
+    xd, wd = gu.to_dev(x, w)
+    want = gu.oracle_full(x, w)
+    for cfg in _launch_settings():
+        rg.rg_linear_set_launch(**cfg) if cfg else rg.rg_linear_set_launch(None)
+        try:
+            plan = rg.rg_plan(M, N, K)
+        except rg.RgError:
+            continue                                # setting not valid for this shape
+        gu.log(f"  launch {cfg} -> {plan['kernel_name']} nw={plan['waves_per_wg']} grid={plan['grid_wgs']}")
+        y = gu.run(xd, wd)
+        torch.cuda.synchronize()
+        gu.assert_bitwise(y.cpu().numpy(), want, f"({M},{N},{K}) launch {cfg}")
+    rg.rg_linear_set_launch(None)
+
+
+def test_cu_masks_do_not_change_bits():
+    import torch
+    import paper_2609_25624_amd as rg
+    ncu = rg.rg_device_cu_count()
+    nwords = (ncu + 31) // 32
+    masks = {
+        "all": [0xFFFFFFFF] * nwords,
+        "half": [0xFFFFFFFF if i < nwords // 2 else 0 for i in range(nwords)],
+        "37": [(1 << 32) - 1 if i == 0 else ((1 << 5) - 1 if i == 1 else 0) for i in range(nwords)],
+        "every8th": [0x01010101] * nwords,
+        "one": [1] + [0] * (nwords - 1),
+    }
+    M, N, K = 1, 6144, 4096
+    x, w = gu.layer(M, N, K, seed=31)
+    xd, wd = gu.to_dev(x, w)
+    want = gu.oracle_full(x, w)
+    for name, mask in masks.items():
+        s = rg.rg_stream_create_cu_mask(mask)
+        try:
+            ext = torch.cuda.ExternalStream(s)
+            y = torch.empty((M, N), dtype=torch.float32, device=gu.dev())
+            torch.cuda.synchronize()
+            gu.run(xd, wd, stream=ext, out=y)
+            ext.synchronize()
+            gu.log(f"  cu mask {name}: done")
+            gu.assert_bitwise(y.cpu().numpy(), want, f"cu mask {name}")
+        finally:
+            torch.cuda.synchronize()
+            rg.rg_stream_destroy(s)
+
+
+def test_fifty_repeats_one_distinct_output():
+    # Supplement C, R3 ablation: ordered split-K returns one result in 50 runs.
+    import torch
+    M, N, K = 1, 4096, 14336
+    x, w = gu.layer(M, N, K, seed=41)
+    xd, wd = gu.to_dev(x, w)
+    outs = torch.empty((50, N), dtype=torch.float32, device=gu.dev())
+    for r in range(50):
+        gu.run(xd, wd, out=outs[r:r + 1])
+    torch.cuda.synchronize()
+    o = outs.cpu().numpy()
+    assert len({o[r].tobytes() for r in range(50)}) == 1
+    gu.assert_bitwise(o[0:1], gu.oracle_full(x, w), "repeat")
+
+
+def test_alternating_inputs_never_see_stale_data():
+    import torch
+    M, N, K = 1, 4096, 4096
+    xa, wa = gu.layer(M, N, K, seed=51)
+    xb, wb = gu.layer(M, N, K, seed=52)
+    da, db = gu.to_dev(xa, wa), gu.to_dev(xb, wb)
+    ya_want, yb_want = gu.oracle_full(xa, wa), gu.oracle_full(xb, wb)
+    outs = []
+    for r in range(10):
+        d = da if r % 2 == 0 else db
+        outs.append(gu.run(*d))
+    torch.cuda.synchronize()
+    for r, y in enumerate(outs):
+        gu.assert_bitwise(y.cpu().numpy(), ya_want if r % 2 == 0 else yb_want, f"alternating call {r}")
+
+
+def test_other_stream_and_concurrent_load():
+    import torch
+    M, N, K = 2, 28672, 4096
+    x, w = gu.layer(M, N, K, seed=61)
+    xd, wd = gu.to_dev(x, w)
+    want = gu.oracle_full(x, w)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    a = torch.randn(4096, 4096, device=gu.dev())
+    torch.cuda.synchronize()
+    ys = []
+    with torch.cuda.stream(s2):
+        for _ in range(8):
+            a = a @ a.t()
+            a = a / a.abs().max()
+    with torch.cuda.stream(s1):
+        for _ in range(4):
+            ys.append(gu.run(xd, wd, stream=s1))
+    torch.cuda.synchronize()
+    for y in ys:
+        gu.assert_bitwise(y.cpu().numpy(), want, "stream under load")
+
+
+def test_cast_kernel_is_the_exact_upcast():
+    import torch
+    import paper_2609_25624_amd as rg
+    rng = np.random.default_rng(3)
+    w = rng.integers(0, 1 << 16, 100003, dtype=np.uint32).astype(np.uint16)
+    wd = torch.from_numpy(w.view(np.int16)).to(gu.dev())
+    out = torch.empty(w.size, dtype=torch.float32, device=gu.dev())
+    rg.rg_cast_bf16_f32(wd, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), w.astype(np.uint32) << 16)
+
+
+def test_argmax_kernel_ties_and_nan():
+    import torch
+    import oracle
+    import paper_2609_25624_amd as rg
+    rows = [
+        [1.0, 3.0, 3.0, 2.0],
+        [-1.0, -0.0, 0.0, -5.0],
+        [float("nan"), 2.0, 2.0, 1.0],
+        [float("nan")] * 4,
+    ]
+    y = torch.tensor(rows, dtype=torch.float32, device=gu.dev())
+    idx = torch.empty(4, dtype=torch.int64, device=gu.dev())
+    rg.rg_argmax_rows(y, idx)
+    torch.cuda.synchronize()
+    assert idx.cpu().tolist() == [1, 1, 1, -1]
+    big = np.full((3, 100000), -1.0, dtype=np.float32)
+    big[0, 99999] = 2.0
+    big[1, [17, 50000, 99999]] = 5.0
+    big[2, :] = 0.0
+    yb = torch.from_numpy(big).to(gu.dev())
+    idx = torch.empty(3, dtype=torch.int64, device=gu.dev())
+    rg.rg_argmax_rows(yb, idx)
+    torch.cuda.synchronize()
+    assert idx.cpu().tolist() == [oracle.argmax(big[i]) for i in range(3)] == [99999, 17, 0]
