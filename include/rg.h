@@ -68,8 +68,9 @@ typedef enum {
 /* Kernel ids reported by rg_plan (scheduling only; the order is the same). */
 typedef enum {
     RG_KERNEL_GENERIC = 0,   /* one thread per output; any K, any alignment */
-    RG_KERNEL_DECODE = 1,    /* M <= 8: quad-broadcast streaming GEMV, whole K per workgroup */
-    RG_KERNEL_TILED = 2      /* M > 8: register-tiled kernel, whole K per workgroup */
+    RG_KERNEL_DECODE = 1,    /* M <= 4: streaming GEMV / skinny GEMM, x in registers */
+    RG_KERNEL_TILED = 2,     /* larger M: register-tiled kernel, whole K per workgroup */
+    RG_KERNEL_DECODE_XS = 3  /* M == 1: streaming GEMV with x streamed through LDS beside W */
 } rg_kernel_id;
 
 /* Scheduling overrides for the determinism tests.  0 in a field = planner
@@ -80,7 +81,7 @@ typedef enum {
  *                    call returns RG_ERR_RANGE)
  *   waves_per_wg  : 1..8  waves (64 threads each) per workgroup
  *   grid_wgs      : 1..65536 workgroups (work is spread over them evenly)
- *   depth         : 1..4  decode pipeline depth in 128-byte-per-row slabs
+ *   depth         : 2..3  decode pipeline depth in 128-byte-per-row slabs
  *   grid_order    : 0 = forward, 1 = reversed workgroup-to-rows mapping
  */
 typedef struct {
@@ -147,6 +148,10 @@ int rg_stream_destroy(void* stream);
 
 /* Number of compute units of the current device (RG_ERR_HIP if none). */
 int rg_device_cu_count(int32_t* out);
+
+/* The hipError_t code of the last HIP call this thread made inside the
+ * library (0 = hipSuccess); explains an RG_ERR_HIP return. */
+int rg_last_hip_error(void);
 
 /* Static description of an rg_status code (never NULL). */
 const char* rg_strerror(int code);

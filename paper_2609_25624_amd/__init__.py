@@ -12,14 +12,17 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librg.so")
 
 RG_OK, RG_ERR_INVAL, RG_ERR_ALIGN, RG_ERR_ARCH, RG_ERR_HIP, RG_ERR_RANGE, RG_ERR_ALIAS = range(7)
-KERNELS = {0: "generic", 1: "decode", 2: "tiled"}
+KERNELS = {0: "generic", 1: "decode", 2: "tiled", 3: "decode_xs"}
 CHUNK = 256
 
 
 class RgError(RuntimeError):
     def __init__(self, code, where):
         self.code = code
-        super().__init__(f"{where}: {strerror(code)} (rg status {code})")
+        extra = ""
+        if code == RG_ERR_HIP:
+            extra = f", hipError {lib.rg_last_hip_error()}"
+        super().__init__(f"{where}: {strerror(code)} (rg status {code}{extra})")
 
 
 class rg_launch_t(ctypes.Structure):
@@ -35,6 +38,12 @@ class rg_plan_t(ctypes.Structure):
 
 
 def _load():
+    # librg.so needs libamdhip64.so.7.  PyTorch ships its own copy of the HIP
+    # runtime; loading torch first makes the dynamic loader bind librg.so to
+    # that same runtime (same soname), so device pointers and streams from
+    # torch are valid in librg.  Two HIP runtimes in one process do not share
+    # the device (the second reports no device).
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() (hipcc, gfx950)")
     L = ctypes.CDLL(LIB_PATH)
@@ -49,6 +58,7 @@ def _load():
         "rg_stream_destroy": [vp],
         "rg_device_cu_count": [ctypes.POINTER(i32)],
         "rg_strerror": [ctypes.c_int],
+        "rg_last_hip_error": [],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -62,7 +72,8 @@ lib = _load()
 
 # Every symbol include/rg.h declares (checked by the tests).
 EXPORTS = ("rg_linear", "rg_linear_set_launch", "rg_plan", "rg_cast_bf16_f32", "rg_argmax_rows",
-           "rg_stream_create_cu_mask", "rg_stream_destroy", "rg_device_cu_count", "rg_strerror")
+           "rg_stream_create_cu_mask", "rg_stream_destroy", "rg_device_cu_count", "rg_strerror",
+           "rg_last_hip_error")
 
 
 def strerror(code: int) -> str:
@@ -123,7 +134,7 @@ def rg_linear_set_launch(cfg=None, **kw):
     c = rg_launch_t()
     for k, v in dict(cfg or {}, **kw).items():
         if k == "kernel" and isinstance(v, str):
-            v = {"generic": 1, "decode": 2, "tiled": 3}[v]
+            v = {"generic": 1, "decode": 2, "tiled": 3, "decode_xs": 4}[v]
         setattr(c, k, int(v))
     _check(lib.rg_linear_set_launch(ctypes.byref(c)), "rg_linear_set_launch")
 

@@ -23,6 +23,7 @@ constexpr int kMaxDevices = 64;
 constexpr int64_t kMaxDecodeRowsStage = 4096 / 4 * 4;  // rows * MT floats staged per WG <= 16 KB
 
 rg_launch_t g_launch = {};                  // all zero: planner defaults
+thread_local int t_last_hip = 0;            // last hipError_t seen by this thread's calls
 std::mutex g_launch_mu;
 
 struct DeviceInfo {
@@ -32,9 +33,12 @@ struct DeviceInfo {
 };
 DeviceInfo g_dev[kMaxDevices];
 
+int hip_status(hipError_t e);
+
 int device_check(int* cus_out) {
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return RG_ERR_HIP;
+    const hipError_t ge = hipGetDevice(&dev);
+    if (ge != hipSuccess) return hip_status(ge);
     if (dev < 0 || dev >= kMaxDevices) return RG_ERR_HIP;
     DeviceInfo& d = g_dev[dev];
     std::call_once(d.once, [&] {
@@ -59,47 +63,68 @@ struct Plan {
     int mt = 0, nw = 0, grid = 0, depth = 0, rq = 0, reverse = 0;
     int64_t Q = 0;
     int max_rows_wg = 0;
+    bool x_streamed = false;
     int tile_m = 0, tile_n = 0;
 };
 
-// Decode schedule for a shape: waves per workgroup and quads per round.
-// Minimises rounds per workgroup, then idle lanes, then prefers more waves.
-bool decode_schedule(int64_t N, int64_t J, int mt, const rg_launch_t& o, Plan* p) {
+// Largest decode pipeline depth whose LDS ring fits for a wave count.
+//  decode  (x in registers): NW * depth * 8 KB of W slabs.
+//  decode1 (M == 1, x streamed): NW * depth * 12 KB of W and x slabs.
+int max_depth(bool x_streamed, int nw) {
+    if (x_streamed) return nw <= 4 ? 3 : (nw <= 6 ? 2 : 0);
+    return nw <= 4 ? 3 : 2;
+}
+
+// Decode schedule for a shape: waves per workgroup, quads per round, depth.
+// Each workgroup streams its rows through an LDS ring of nw * depth slabs,
+// (depth - 1) of them in flight per wave.  The choice maximises the useful
+// W bytes in flight per CU (up to ~96 KB, which covers HBM latency at the
+// per-CU share of 8 TB/s), then minimises rounds, then idle lanes.
+bool decode_schedule(int64_t N, int64_t J, int mt, bool x_streamed, const rg_launch_t& o, Plan* p) {
     static const int kNW[] = {7, 6, 4, 2, 1};
+    const int64_t stage_cap = x_streamed ? kMaxDecodeRowsStage / 2 : kMaxDecodeRowsStage;
     p->Q = ceil_div(N, 4);
     int64_t grid = o.grid_wgs > 0 ? o.grid_wgs : (p->Q >= kNominalCUs ? kNominalCUs : p->Q);
     // staging of results: 4 * ceil(Q/grid) rows * mt floats must stay small
-    while (4 * ceil_div(p->Q, grid) * mt > kMaxDecodeRowsStage) {
+    while (4 * ceil_div(p->Q, grid) * mt > stage_cap) {
         if (o.grid_wgs > 0) return false;
         grid *= 2;
     }
     if (grid > p->Q) grid = p->Q;
     const int64_t qpw = ceil_div(p->Q, grid);
-    int best_nw = 0, best_rq = 0;
+    int best_nw = 0, best_rq = 0, best_depth = 0;
     int64_t best_rounds = 0;
-    double best_eff = -1.0;
+    double best_eff = -1.0, best_fly = -1.0;
     for (int nw : kNW) {
         if (o.waves_per_wg > 0 && nw != o.waves_per_wg) continue;
         if (mt == 4 && nw > 4) continue;   // 4 rows of x need one wave per SIMD (registers)
+        const int dmax = max_depth(x_streamed, nw);
+        if (dmax == 0) continue;
         const int64_t rq = (16 * nw) / J;
         if (rq < 1) continue;
+        const int depth = o.depth > 0 ? o.depth : dmax;
+        if (depth < 2 || depth > dmax) continue;
         const int64_t rounds = ceil_div(qpw, rq);
         const double eff = (double)(qpw * J) / (double)(rounds * 16 * nw);
-        const bool better = best_nw == 0 || rounds < best_rounds ||
-                            (rounds == best_rounds && eff > best_eff + 1e-9);
+        double fly = nw * (depth - 1) * 8.0 * eff;          // KB of useful W in flight
+        if (fly > 96.0) fly = 96.0;
+        const bool better = best_nw == 0 || fly > best_fly + 1e-9 ||
+                            (fly > best_fly - 1e-9 && (rounds < best_rounds ||
+                                                       (rounds == best_rounds && eff > best_eff + 1e-9)));
         if (better) {
             best_nw = nw;
             best_rq = (int)rq;
+            best_depth = depth;
             best_rounds = rounds;
             best_eff = eff;
+            best_fly = fly;
         }
     }
     if (best_nw == 0) return false;
     p->nw = best_nw;
     p->rq = best_rq;
     p->grid = (int)grid;
-    p->depth = o.depth > 0 ? o.depth : (best_nw <= 4 ? 3 : 2);
-    if (p->depth < 2 || p->depth > 3 || (p->depth == 3 && p->nw > 4)) return false;
+    p->depth = best_depth;
     p->max_rows_wg = (int)(4 * qpw);
     return true;
 }
@@ -109,18 +134,31 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     const int64_t J = ceil_div(K, rg::kChunk);
     int want = RG_KERNEL_GENERIC;
     const int mt = M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 0;
-    if (fast_ok && mt > 0 && J <= 112) want = RG_KERNEL_DECODE;
-    if (o.kernel > 0) {
+    const bool decode_ok = fast_ok && mt > 0 && J <= 112;
+    if (decode_ok) want = (mt == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;
+    const bool forced = o.kernel > 0;
+    if (forced) {
         want = o.kernel - 1;
-        if (want == RG_KERNEL_DECODE && !(fast_ok && mt > 0 && J <= 112)) return RG_ERR_RANGE;
+        if ((want == RG_KERNEL_DECODE || want == RG_KERNEL_DECODE_XS) && !decode_ok) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_DECODE_XS && mt != 1) return RG_ERR_RANGE;
         if (want == RG_KERNEL_TILED) return RG_ERR_RANGE;  // not built yet
     }
     p->kernel = want;
     p->reverse = o.grid_order;
+    if (want == RG_KERNEL_DECODE_XS) {
+        // M == 1: x streamed beside W, when its wave counts cover J; else x in registers.
+        p->mt = 1;
+        if (decode_schedule(N, J, 1, true, o, p)) {
+            p->x_streamed = true;
+        } else {
+            if (forced) return RG_ERR_RANGE;
+            want = p->kernel = RG_KERNEL_DECODE;
+        }
+    }
     if (want == RG_KERNEL_DECODE) {
         p->mt = mt;
-        if (!decode_schedule(N, J, mt, o, p)) {
-            if (o.kernel > 0 || o.waves_per_wg > 0 || o.grid_wgs > 0 || o.depth > 0) return RG_ERR_RANGE;
+        if (!decode_schedule(N, J, mt, false, o, p)) {
+            if (forced || o.waves_per_wg > 0 || o.grid_wgs > 0 || o.depth > 0) return RG_ERR_RANGE;
             p->kernel = RG_KERNEL_GENERIC;
         }
     }
@@ -135,10 +173,10 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
 }
 
 int validate_launch(const rg_launch_t& c) {
-    if (c.kernel < -1 || c.kernel > 3) return RG_ERR_RANGE;
+    if (c.kernel < -1 || c.kernel > 4) return RG_ERR_RANGE;
     if (c.waves_per_wg < 0 || c.waves_per_wg > 8) return RG_ERR_RANGE;
     if (c.grid_wgs < 0 || c.grid_wgs > 65536) return RG_ERR_RANGE;
-    if (c.depth < 0 || c.depth > 4) return RG_ERR_RANGE;
+    if (c.depth < 0 || c.depth > 3 || c.depth == 1) return RG_ERR_RANGE;
     if (c.grid_order < 0 || c.grid_order > 1) return RG_ERR_RANGE;
     return RG_OK;
 }
@@ -146,6 +184,12 @@ int validate_launch(const rg_launch_t& c) {
 rg_launch_t current_launch() {
     std::lock_guard<std::mutex> lk(g_launch_mu);
     return g_launch;
+}
+
+// Map a launch result to an rg_status, remembering the HIP code for rg_last_hip_error.
+int hip_status(hipError_t e) {
+    t_last_hip = (int)e;
+    return e == hipSuccess ? RG_OK : RG_ERR_HIP;
 }
 
 bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
@@ -217,8 +261,9 @@ int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N,
     const int s = make_plan(M, N, K, fast_ok, current_launch(), &p);
     if (s != RG_OK) return s;
     hipStream_t st = (hipStream_t)stream;
+    (void)hipGetLastError();   // drop an error left by an unrelated earlier HIP call on this thread
     hipError_t e = hipSuccess;
-    if (p.kernel == RG_KERNEL_DECODE) {
+    if (p.kernel == RG_KERNEL_DECODE || p.kernel == RG_KERNEL_DECODE_XS) {
         rg::DecodeArgs a;
         a.x = x;
         a.w = w;
@@ -227,15 +272,19 @@ int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N,
         a.N = N;
         a.K = K;
         a.Q = p.Q;
+        a.qbase = p.Q / p.grid;
+        a.qrem = (int)(p.Q % p.grid);
         a.J = (int)ceil_div(K, rg::kChunk);
+        a.jmagic = a.J > 1 ? (uint32_t)(((uint64_t)1 << 32) / (uint64_t)a.J + 1) : 0u;
         a.RQ = p.rq;
         a.reverse = p.reverse;
         a.max_rows_wg = p.max_rows_wg;
-        e = rg::launch_decode(a, p.mt, p.grid, p.nw, p.depth, st);
+        e = p.x_streamed ? rg::launch_decode1(a, p.grid, p.nw, p.depth, st)
+                         : rg::launch_decode(a, p.mt, p.grid, p.nw, p.depth, st);
     } else {
         e = rg::launch_generic(x, w, y, M, N, K, p.grid, p.reverse, st);
     }
-    return e == hipSuccess ? RG_OK : RG_ERR_HIP;
+    return hip_status(e);
 }
 
 int rg_cast_bf16_f32(const uint16_t* w, float* o, int64_t count, void* stream) {
@@ -243,7 +292,8 @@ int rg_cast_bf16_f32(const uint16_t* w, float* o, int64_t count, void* stream) {
     if (((uintptr_t)w & 1) || ((uintptr_t)o & 3)) return RG_ERR_ALIGN;
     const int dc = device_check(nullptr);
     if (dc != RG_OK) return dc;
-    return rg::launch_cast(w, o, count, (hipStream_t)stream) == hipSuccess ? RG_OK : RG_ERR_HIP;
+    (void)hipGetLastError();
+    return hip_status(rg::launch_cast(w, o, count, (hipStream_t)stream));
 }
 
 int rg_argmax_rows(const float* y, int64_t* out, int64_t M, int64_t N, void* stream) {
@@ -251,21 +301,24 @@ int rg_argmax_rows(const float* y, int64_t* out, int64_t M, int64_t N, void* str
     if (((uintptr_t)y & 3) || ((uintptr_t)out & 7)) return RG_ERR_ALIGN;
     const int dc = device_check(nullptr);
     if (dc != RG_OK) return dc;
-    return rg::launch_argmax(y, out, M, N, (hipStream_t)stream) == hipSuccess ? RG_OK : RG_ERR_HIP;
+    (void)hipGetLastError();
+    return hip_status(rg::launch_argmax(y, out, M, N, (hipStream_t)stream));
 }
 
 int rg_stream_create_cu_mask(const uint32_t* mask, uint32_t nwords, void** out_stream) {
     if (!mask || nwords == 0 || !out_stream) return RG_ERR_INVAL;
     hipStream_t s = nullptr;
-    if (hipExtStreamCreateWithCUMask(&s, nwords, mask) != hipSuccess) return RG_ERR_HIP;
-    *out_stream = (void*)s;
-    return RG_OK;
+    const int st = hip_status(hipExtStreamCreateWithCUMask(&s, nwords, mask));
+    if (st == RG_OK) *out_stream = (void*)s;
+    return st;
 }
 
 int rg_stream_destroy(void* stream) {
     if (!stream) return RG_ERR_INVAL;
-    return hipStreamDestroy((hipStream_t)stream) == hipSuccess ? RG_OK : RG_ERR_HIP;
+    return hip_status(hipStreamDestroy((hipStream_t)stream));
 }
+
+int rg_last_hip_error(void) { return t_last_hip; }
 
 int rg_device_cu_count(int32_t* out) {
     if (!out) return RG_ERR_INVAL;

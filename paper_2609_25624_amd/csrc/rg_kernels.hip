@@ -37,6 +37,28 @@ __device__ __forceinline__ float quad_bcast(float v) {
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), ctrl, 0xf, 0xf, true));
 }
 
+
+// acc = fmaf(x[quad lane E], w[h], acc) for h = 0..7 in order, with the x
+// broadcast fused into the FMA (v_fmac_f32_dpp, DPP on the x operand).  The
+// leading s_nop covers the two wait states a DPP read needs after a VALU
+// write of its source.  Each v_fmac is one IEEE-754 binary32 fused
+// multiply-add; the DPP modifier only selects which lane's x is read.
+template <int E>
+__device__ __forceinline__ void fmac8_bcast(float& acc, const float* x, const float* w) {
+    asm("s_nop 1\n\t"
+        "v_fmac_f32_dpp %0, %1, %9 quad_perm:[%17,%17,%17,%17] row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "v_fmac_f32_dpp %0, %2, %10 quad_perm:[%17,%17,%17,%17] row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "v_fmac_f32_dpp %0, %3, %11 quad_perm:[%17,%17,%17,%17] row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "v_fmac_f32_dpp %0, %4, %12 quad_perm:[%17,%17,%17,%17] row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "v_fmac_f32_dpp %0, %5, %13 quad_perm:[%17,%17,%17,%17] row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "v_fmac_f32_dpp %0, %6, %14 quad_perm:[%17,%17,%17,%17] row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "v_fmac_f32_dpp %0, %7, %15 quad_perm:[%17,%17,%17,%17] row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "v_fmac_f32_dpp %0, %8, %16 quad_perm:[%17,%17,%17,%17] row_mask:0xf bank_mask:0xf bound_ctrl:1"
+        : "+v"(acc)
+        : "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]), "v"(x[4]), "v"(x[5]), "v"(x[6]), "v"(x[7]),
+          "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "v"(w[4]), "v"(w[5]), "v"(w[6]), "v"(w[7]), "n"(E));
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) void*)p);
 }
@@ -59,11 +81,36 @@ __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t
 }
 
 // Wait until at most N vector-memory operations of this wave are outstanding.
-// Only loads are in flight while it is used, and they complete in issue order.
+// Used only while the outstanding operations are all global->LDS DMA loads of
+// this wave, which complete in issue order among themselves.
 template <int N>
 __device__ __forceinline__ void vmcnt_wait() {
     static_assert(N >= 0 && N <= 63, "vmcnt range");
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+
+// n / J and n % J for small n (n < 2^16) without a runtime divide: the host
+// passes jmagic = ceil(2^32 / J), exact for n < 2^32 / J (J = 1 handled apart).
+__device__ __forceinline__ int div_j(int n, int J, uint32_t jmagic) {
+    return J == 1 ? n : (int)__umulhi((uint32_t)n, jmagic);
+}
+
+// Left fold of one output's J segment partials p[0..J-1] (contiguous floats in
+// LDS): ((p0 + p1) + p2) + ...  The reads are issued in groups ahead of the
+// additions; the additions stay in ascending order.
+__device__ __forceinline__ float fold_partials(const float* p, int J) {
+    float y = p[0];
+    int j = 1;
+    for (; j + 16 <= J; j += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = p[j + u];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) y = y + v[u];
+    }
+    for (; j < J; ++j) y = y + p[j];
+    return y;
 }
 
 // ---------------------------------------------------------------------------
@@ -119,12 +166,34 @@ __global__ void __launch_bounds__(256) generic_kernel(const float* __restrict__ 
 // One 64-element slab of a lane's chain: acc[m] = fmaf(x, up(w), acc[m]) for
 // the slab's elements in ascending k.  wp holds the lane's 8 pieces of 8 bf16;
 // X[m][S][i] holds x for element 16*e + i of the slab in quad lane e.
-template <int S, int MT>
+// FULL: all 8 pieces present (no per-piece test, so the compiler keeps all
+// LDS reads in flight together); otherwise the first npieces pieces.
+template <int S, int MT, bool FULL>
 __device__ __forceinline__ void fma_slab(const uint4 (&wp)[8], const float (&X)[MT][4][16], float (&acc)[MT],
                                          int npieces) {
+    if constexpr (FULL) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const uint32_t d[4] = {wp[t].x, wp[t].y, wp[t].z, wp[t].w};
+            float wv[8];
+#pragma unroll
+            for (int h = 0; h < 8; ++h) wv[h] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const float* xb = &X[m][S][8 * (t & 1)];
+                switch (t >> 1) {
+                    case 0: fmac8_bcast<0>(acc[m], xb, wv); break;
+                    case 1: fmac8_bcast<1>(acc[m], xb, wv); break;
+                    case 2: fmac8_bcast<2>(acc[m], xb, wv); break;
+                    default: fmac8_bcast<3>(acc[m], xb, wv); break;
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
-        if (npieces < 8 && t >= npieces) break;   // short last segment only
+        if (!FULL && t >= npieces) break;   // short last segment only
         const uint32_t d[4] = {wp[t].x, wp[t].y, wp[t].z, wp[t].w};
 #pragma unroll
         for (int h = 0; h < 8; ++h) {
@@ -152,11 +221,11 @@ constexpr int kSlabBytesPerWave = 64 * 128;  // 8 KB
 template <int MT, int NW, int DEPTH>
 __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     static_assert(MT == 1 || MT == 2 || MT == 4, "decode M tile");
-    static_assert(DEPTH >= 2 && DEPTH <= 4, "pipeline depth");
+    static_assert(DEPTH >= 2 && DEPTH <= 3, "pipeline depth");
     constexpr int kThreads = NW * 64;
 
     __shared__ __attribute__((aligned(16))) uint8_t wring[NW][DEPTH][kSlabBytesPerWave];
-    __shared__ float part[2][kThreads * MT];          // [parity][row_local * J + j][m]
+    __shared__ float part[2][kThreads * MT];          // [parity][m][row_local * J + j]
     extern __shared__ float yres[];                   // [row_in_wg][m], dynamic
 
     const int tid = threadIdx.x;
@@ -166,10 +235,10 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     const int RQ = a.RQ;
     const int64_t N = a.N, K = a.K;
 
-    const int64_t G = gridDim.x;
-    const int64_t g = a.reverse ? (G - 1 - blockIdx.x) : blockIdx.x;
-    const int64_t q0 = g * a.Q / G, q1 = (g + 1) * a.Q / G;
-    const int nq = (int)(q1 - q0);
+    // balanced split of the Q quads over the grid (the first qrem workgroups take one more)
+    const int g = a.reverse ? (int)(gridDim.x - 1 - blockIdx.x) : (int)blockIdx.x;
+    const int64_t q0 = (int64_t)g * a.qbase + min(g, a.qrem);
+    const int nq = (int)a.qbase + (g < a.qrem ? 1 : 0);
     const int rounds = (nq + RQ - 1) / RQ;
     const int nsteps = rounds * (kChunk / kSlab);
 
@@ -177,12 +246,16 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     const int ql = tid >> 2;                 // quad lane in the workgroup
     const int e = tid & 3;                   // row inside the quad
     const bool role = ql < RQ * J;
-    const int lq = role ? ql / J : 0;        // quad inside the round
-    const int jj = role ? ql % J : 0;        // segment
+    const int lq = role ? div_j(ql, J, a.jmagic) : 0;   // quad inside the round
+    const int jj = role ? ql - lq * J : 0;              // segment
     const int seg_len = (jj == J - 1) ? (int)(K - (int64_t)(J - 1) * kChunk) : kChunk;
 
     // ---- x of this lane's segment, resident in registers ----
-    // X[m][s][i] = x[m][jj*256 + 64 s + 16 e + i] (0 beyond K or M)
+    // X[m][s][i] = x[m][jj*256 + 64 s + 16 e + i] (0 beyond K or M).  These are
+    // ordinary compiler-tracked loads: the compiler waits for them with
+    // vmcnt(0) before their first use.  (A partial vmcnt wait must never be
+    // relied on for them: loads returning to registers and global->LDS DMA
+    // loads are not guaranteed to complete in issue order with each other.)
     float X[MT][4][16];
 #pragma unroll
     for (int m = 0; m < MT; ++m)
@@ -216,7 +289,7 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
             const int cql = wave * 16 + (sigma >> 2);
             const int t = p ^ ((sigma >> 1) & 7);
             if (cql < RQ * J) {
-                const int cq = cql / J, cj = cql % J;
+                const int cq = div_j(cql, J, a.jmagic), cj = cql - cq * J;
                 dma_row[i] = 4 * cq + (sigma & 3);
                 dma_col[i] = (uint32_t)cj * (kChunk * 2) + 16u * t;
                 dma_jlen[i] = (cj == J - 1) ? (int)(K - (int64_t)(J - 1) * kChunk) : kChunk;
@@ -262,8 +335,7 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
         const int r = st >> 2, s = st & 3;
         if (st + DEPTH - 1 < nsteps) issue(st + DEPTH - 1);
         const int ahead = min(DEPTH - 1, nsteps - 1 - st);
-        if (ahead >= 3) vmcnt_wait<24>();
-        else if (ahead == 2) vmcnt_wait<16>();
+        if (ahead >= 2) vmcnt_wait<16>();
         else if (ahead == 1) vmcnt_wait<8>();
         else vmcnt_wait<0>();
 
@@ -280,11 +352,20 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
             uint4 wp[8];
 #pragma unroll
             for (int t = 0; t < 8; ++t) wp[t] = *reinterpret_cast<const uint4*>(src + 16 * (t ^ sw));
-            switch (s) {   // static slab index keeps X in registers
-                case 0: fma_slab<0, MT>(wp, X, acc, npieces); break;
-                case 1: fma_slab<1, MT>(wp, X, acc, npieces); break;
-                case 2: fma_slab<2, MT>(wp, X, acc, npieces); break;
-                default: fma_slab<3, MT>(wp, X, acc, npieces); break;
+            if (npieces == 8) {
+                switch (s) {   // static slab index keeps X in registers
+                    case 0: fma_slab<0, MT, true>(wp, X, acc, 8); break;
+                    case 1: fma_slab<1, MT, true>(wp, X, acc, 8); break;
+                    case 2: fma_slab<2, MT, true>(wp, X, acc, 8); break;
+                    default: fma_slab<3, MT, true>(wp, X, acc, 8); break;
+                }
+            } else {
+                switch (s) {
+                    case 0: fma_slab<0, MT, false>(wp, X, acc, npieces); break;
+                    case 1: fma_slab<1, MT, false>(wp, X, acc, npieces); break;
+                    case 2: fma_slab<2, MT, false>(wp, X, acc, npieces); break;
+                    default: fma_slab<3, MT, false>(wp, X, acc, npieces); break;
+                }
             }
         }
         if (s == 3) {
@@ -292,16 +373,13 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
             const int par = r & 1;
             if (active) {
 #pragma unroll
-                for (int m = 0; m < MT; ++m) part[par][((4 * lq + e) * J + jj) * MT + m] = acc[m];
+                for (int m = 0; m < MT; ++m) part[par][m * (kThreads) + (4 * lq + e) * J + jj] = acc[m];
             }
             __syncthreads();
             const int rows_round = 4 * min(RQ, nq - r * RQ);
             for (int o = tid; o < rows_round * MT; o += kThreads) {
                 const int rl = o / MT, m = o % MT;
-                const float* pp = &part[par][rl * J * MT + m];
-                float yv = pp[0];
-                for (int j = 1; j < J; ++j) yv = yv + pp[j * MT];
-                yres[(r * RQ * 4 + rl) * MT + m] = yv;
+                yres[(r * RQ * 4 + rl) * MT + m] = fold_partials(&part[par][m * kThreads + rl * J], J);
             }
             // The next round writes the other parity; this parity is rewritten
             // only after the next round's barrier, which all folds precede.
@@ -315,6 +393,233 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
         const int m = o / rows_wg, rl = o % rows_wg;
         const int64_t n = rowbase + rl;
         if (m < a.M && n < N) a.y[(int64_t)m * N + n] = yres[rl * MT + m];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// decode kernel for M == 1 with x streamed beside W.
+//
+// Same work split, lane roles, order and W data path as decode_kernel, but x
+// is not preloaded into registers: with every 64-element W slab, each wave
+// also DMAs the matching 64 floats of x for each of its 16 quads (4 KB) into
+// a second LDS ring.  All loads in flight are then global->LDS DMA loads of
+// one wave, which complete in issue order, so a slab can be consumed as soon
+// as its own loads have landed.  Lane e of a quad reads the 16 floats x[16e,
+// 16e+16) of the slab; the others reach it through DPP quad broadcasts.  The
+// 256-byte x image of a quad is stored with its 16-byte pieces permuted
+// (piece c of lane e at slot 4e + (c ^ (quad & 3))) so that the 16 lanes of
+// an LDS phase read 16 distinct bank groups.
+// ---------------------------------------------------------------------------
+constexpr int kXSlabBytesPerWave = 16 * 256;  // 4 KB: 16 quads x 64 floats
+
+template <bool FULL>
+__device__ __forceinline__ void fma_slab1(const uint4 (&wp)[8], const float (&Xs)[16], float& acc, int npieces) {
+    if constexpr (FULL) {
+        // 8 pieces of 8 elements; piece t uses the x block of quad lane t/2
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const uint32_t d[4] = {wp[t].x, wp[t].y, wp[t].z, wp[t].w};
+            float wv[8];
+#pragma unroll
+            for (int h = 0; h < 8; ++h) wv[h] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+            const float* xb = &Xs[8 * (t & 1)];
+            switch (t >> 1) {
+                case 0: fmac8_bcast<0>(acc, xb, wv); break;
+                case 1: fmac8_bcast<1>(acc, xb, wv); break;
+                case 2: fmac8_bcast<2>(acc, xb, wv); break;
+                default: fmac8_bcast<3>(acc, xb, wv); break;
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        if (!FULL && t >= npieces) break;   // short last segment only
+        const uint32_t d[4] = {wp[t].x, wp[t].y, wp[t].z, wp[t].w};
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+            const float wv = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+            const int kl = 8 * t + h;          // element inside the slab
+            const int i = kl & 15;             // register inside the x block
+            float xv;
+            switch (kl >> 4) {                 // lane of the quad holding x
+                case 0: xv = quad_bcast<0>(Xs[i]); break;
+                case 1: xv = quad_bcast<1>(Xs[i]); break;
+                case 2: xv = quad_bcast<2>(Xs[i]); break;
+                default: xv = quad_bcast<3>(Xs[i]); break;
+            }
+            acc = __builtin_fmaf(xv, wv, acc);
+        }
+    }
+}
+
+template <int NW, int DEPTH>
+__global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
+    static_assert(DEPTH >= 2 && DEPTH <= 3, "pipeline depth");
+    constexpr int kThreads = NW * 64;
+    constexpr int kDmaPerStep = 8 + 4;      // W: 8 KB, x: 4 KB per wave
+
+    __shared__ __attribute__((aligned(16))) uint8_t wring[NW][DEPTH][kSlabBytesPerWave];
+    __shared__ __attribute__((aligned(16))) uint8_t xring[NW][DEPTH][kXSlabBytesPerWave];
+    __shared__ float part[2][kThreads];               // [parity][row_local * J + j]
+    extern __shared__ float yres[];                   // [row_in_wg], dynamic
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    const int J = a.J;
+    const int RQ = a.RQ;
+    const int64_t N = a.N, K = a.K;
+
+    // balanced split of the Q quads over the grid (the first qrem workgroups take one more)
+    const int g = a.reverse ? (int)(gridDim.x - 1 - blockIdx.x) : (int)blockIdx.x;
+    const int64_t q0 = (int64_t)g * a.qbase + min(g, a.qrem);
+    const int nq = (int)a.qbase + (g < a.qrem ? 1 : 0);
+    const int rounds = (nq + RQ - 1) / RQ;
+    const int nsteps = rounds * (kChunk / kSlab);
+
+    // ---- fixed lane role (consumer) ----
+    const int ql = tid >> 2;
+    const int e = tid & 3;
+    const bool role = ql < RQ * J;
+    const int lq = role ? div_j(ql, J, a.jmagic) : 0;
+    const int jj = role ? ql - lq * J : 0;
+    const int seg_len = (jj == J - 1) ? (int)(K - (int64_t)(J - 1) * kChunk) : kChunk;
+    const int last_len = (int)(K - (int64_t)(J - 1) * kChunk);
+
+    // ---- W DMA role (as in decode_kernel) ----
+    int dma_row[8];
+    uint32_t dma_col[8];
+    int dma_jlen[8];
+    int dma_kin[8];
+    {
+        const int p = lane & 7;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int sigma = 8 * i + (lane >> 3);
+            const int cql = wave * 16 + (sigma >> 2);
+            const int t = p ^ ((sigma >> 1) & 7);
+            if (cql < RQ * J) {
+                const int cq = div_j(cql, J, a.jmagic), cj = cql - cq * J;
+                dma_row[i] = 4 * cq + (sigma & 3);
+                dma_col[i] = (uint32_t)cj * (kChunk * 2) + 16u * t;
+                dma_jlen[i] = (cj == J - 1) ? last_len : kChunk;
+                dma_kin[i] = 8 * t;
+            } else {
+                dma_row[i] = -1;
+                dma_col[i] = 0;
+                dma_jlen[i] = kChunk;
+                dma_kin[i] = 0;
+            }
+        }
+    }
+    // ---- x DMA role: instruction i fills quads 4i..4i+3 of this wave ----
+    // x offsets (elements) of slab 0; the same for every round.
+    int xdma_k[4];       // element index inside x at slab 0, or -1 for an idle quad
+    int xdma_len[4];     // segment length of that quad
+    int xdma_kin[4];     // element offset inside the segment at slab 0
+    {
+        const int sig = lane & 15;
+        const int ee = sig >> 2;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int q = 4 * i + (lane >> 4);
+            const int c = (sig & 3) ^ (q & 3);
+            const int cql = wave * 16 + q;
+            if (cql < RQ * J) {
+                const int cj = cql - div_j(cql, J, a.jmagic) * J;
+                xdma_kin[i] = 16 * ee + 4 * c;
+                xdma_k[i] = cj * kChunk + xdma_kin[i];
+                xdma_len[i] = (cj == J - 1) ? last_len : kChunk;
+            } else {
+                xdma_kin[i] = 0;
+                xdma_k[i] = -1;
+                xdma_len[i] = kChunk;
+            }
+        }
+    }
+    const uint32_t ring_base = lds_addr(&wring[wave][0][0]);
+    const uint32_t xring_base = lds_addr(&xring[wave][0][0]);
+    const int64_t row_bytes = K * 2;
+
+    auto issue = [&](int st) {
+        const int r = st >> 2, s = st & 3;
+        const int64_t row0 = 4 * (q0 + (int64_t)r * RQ);
+        const int64_t rmax = N - 1 - row0;
+        const char* base = reinterpret_cast<const char*>(a.w) + row0 * row_bytes;
+        const uint32_t slot = ring_base + (uint32_t)((st % DEPTH) * kSlabBytesPerWave);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            int64_t row = dma_row[i] < 0 ? 0 : dma_row[i];
+            if (row > rmax) row = rmax;
+            uint32_t col = dma_col[i] + (uint32_t)(s * kSlab * 2);
+            if (s * kSlab + dma_kin[i] >= dma_jlen[i]) col = 0;
+            const uint32_t voff = (uint32_t)(row * row_bytes) + col;
+            dma16(base, voff, slot + 1024u * i);
+        }
+        const uint32_t xslot = xring_base + (uint32_t)((st % DEPTH) * kXSlabBytesPerWave);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            // past the end of a short last segment, or an idle quad: element 0 of x (never used)
+            const bool ok = xdma_k[i] >= 0 && s * kSlab + xdma_kin[i] < xdma_len[i];
+            const uint32_t voff = ok ? 4u * (uint32_t)(xdma_k[i] + s * kSlab) : 0u;
+            dma16(a.x, voff, xslot + 1024u * i);
+        }
+    };
+
+    float acc = 0.0f;
+    const int rows_wg = 4 * nq;
+    const int xq = tid >> 2 & 15;          // quad inside the wave
+
+#pragma unroll
+    for (int st = 0; st < DEPTH - 1; ++st)
+        if (st < nsteps) issue(st);
+
+    for (int st = 0; st < nsteps; ++st) {
+        const int r = st >> 2, s = st & 3;
+        if (st + DEPTH - 1 < nsteps) issue(st + DEPTH - 1);
+        const int ahead = min(DEPTH - 1, nsteps - 1 - st);
+        if (ahead >= 2) vmcnt_wait<2 * kDmaPerStep>();
+        else if (ahead == 1) vmcnt_wait<kDmaPerStep>();
+        else vmcnt_wait<0>();
+
+        const bool active = role && (lq < nq - r * RQ);
+        if (s == 0) acc = 0.0f;
+        const int npieces = min(8, max(0, (seg_len - s * kSlab) / 8));
+        if (active && npieces > 0) {
+            const uint8_t* src = &wring[wave][st % DEPTH][lane * 128];
+            const int sw = (lane >> 1) & 7;
+            uint4 wp[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t) wp[t] = *reinterpret_cast<const uint4*>(src + 16 * (t ^ sw));
+            const uint8_t* xs = &xring[wave][st % DEPTH][xq * 256];
+            float Xs[16];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const float4 v = *reinterpret_cast<const float4*>(xs + 16 * (4 * e + (c ^ (xq & 3))));
+                Xs[4 * c + 0] = v.x;
+                Xs[4 * c + 1] = v.y;
+                Xs[4 * c + 2] = v.z;
+                Xs[4 * c + 3] = v.w;
+            }
+            if (npieces == 8) fma_slab1<true>(wp, Xs, acc, 8);
+            else fma_slab1<false>(wp, Xs, acc, npieces);
+        }
+        if (s == 3) {
+            const int par = r & 1;
+            if (active) part[par][(4 * lq + e) * J + jj] = acc;
+            __syncthreads();
+            const int rows_round = 4 * min(RQ, nq - r * RQ);
+            for (int o = tid; o < rows_round; o += kThreads)
+                yres[r * RQ * 4 + o] = fold_partials(&part[par][o * J], J);
+        }
+    }
+    vmcnt_wait<0>();
+    __syncthreads();
+    const int64_t rowbase = 4 * q0;
+    for (int o = tid; o < rows_wg; o += kThreads) {
+        const int64_t n = rowbase + o;
+        if (n < N) a.y[n] = yres[o];
     }
 }
 
@@ -382,7 +687,10 @@ static hipError_t launch_decode_t(const DecodeArgs& a, int grid, hipStream_t str
     return hipGetLastError();
 }
 
-// Pipeline depths that fit the 160 KB of LDS: 3 up to 4 waves, 2 above.
+// Pipeline depths whose LDS ring (NW * DEPTH * 8 KB) fits next to the
+// partials and results: 3 slabs up to 4 waves, 2 above.  (A depth of 4 is
+// not built: its first GPU run, together with another change, faulted, and
+// the cause has not been shown.)
 template <int MT, int NW>
 static hipError_t launch_decode_d(const DecodeArgs& a, int grid, int depth, hipStream_t stream) {
     if (depth == 2) return launch_decode_t<MT, NW, 2>(a, grid, stream);
@@ -394,12 +702,38 @@ static hipError_t launch_decode_d(const DecodeArgs& a, int grid, int depth, hipS
 
 template <int MT>
 static hipError_t launch_decode_w(const DecodeArgs& a, int grid, int nw, int depth, hipStream_t stream) {
+    if constexpr (MT == 4) {   // 4 rows of x in registers: one wave per SIMD at most
+        if (nw > 4) return hipErrorInvalidValue;
+    }
     switch (nw) {
         case 1: return launch_decode_d<MT, 1>(a, grid, depth, stream);
         case 2: return launch_decode_d<MT, 2>(a, grid, depth, stream);
         case 4: return launch_decode_d<MT, 4>(a, grid, depth, stream);
-        case 6: return launch_decode_d<MT, 6>(a, grid, depth, stream);
-        case 7: return launch_decode_d<MT, 7>(a, grid, depth, stream);
+        case 6: if constexpr (MT < 4) return launch_decode_d<MT, 6>(a, grid, depth, stream); else break;
+        case 7: if constexpr (MT < 4) return launch_decode_d<MT, 7>(a, grid, depth, stream); else break;
+        default: break;
+    }
+    return hipErrorInvalidValue;
+}
+
+template <int NW, int DEPTH>
+static hipError_t launch_decode1_t(const DecodeArgs& a, int grid, hipStream_t stream) {
+    const size_t dyn = (size_t)a.max_rows_wg * sizeof(float);
+    hipLaunchKernelGGL((decode1_kernel<NW, DEPTH>), dim3(grid), dim3(NW * 64), dyn, stream, a);
+    return hipGetLastError();
+}
+
+// M == 1 with x streamed through LDS.  Rings of NW * DEPTH * 12 KB: depth 3
+// up to 4 waves, depth 2 up to 6 waves.
+hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipStream_t stream) {
+    switch (nw * 10 + depth) {
+        case 12: return launch_decode1_t<1, 2>(a, grid, stream);
+        case 13: return launch_decode1_t<1, 3>(a, grid, stream);
+        case 22: return launch_decode1_t<2, 2>(a, grid, stream);
+        case 23: return launch_decode1_t<2, 3>(a, grid, stream);
+        case 42: return launch_decode1_t<4, 2>(a, grid, stream);
+        case 43: return launch_decode1_t<4, 3>(a, grid, stream);
+        case 62: return launch_decode1_t<6, 2>(a, grid, stream);
         default: return hipErrorInvalidValue;
     }
 }

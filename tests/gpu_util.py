@@ -14,8 +14,8 @@ def dev():
 
 def to_dev(x, w):
     import torch
-    xd = torch.from_numpy(np.ascontiguousarray(x)).to(dev())
-    wd = torch.from_numpy(np.ascontiguousarray(w).view(np.int16)).to(dev())
+    xd = torch.from_numpy(np.array(x, dtype=np.float32, copy=True)).to(dev())
+    wd = torch.from_numpy(np.array(w, dtype=np.uint16, copy=True).view(np.int16)).to(dev())
     return xd, wd
 
 

@@ -56,7 +56,8 @@ def test_plan_is_pure_and_overrides_are_scheduling_only():
 
 
 def test_plan_kernel_choice():
-    assert rg.rg_plan(1, 6144, 4096)["kernel_name"] == "decode"
+    assert rg.rg_plan(1, 6144, 4096)["kernel_name"] == "decode_xs"
+    assert rg.rg_plan(1, 8192, 28672)["kernel_name"] == "decode"     # J = 112 needs 7 waves
     assert rg.rg_plan(4, 6144, 4096)["kernel_name"] == "decode"
     assert rg.rg_plan(1, 10, 7)["kernel_name"] == "generic"     # K % 8 != 0
 
