@@ -21,6 +21,7 @@ namespace {
 constexpr int kNominalCUs = 256;            // MI355X; scheduling only
 constexpr int kMaxDevices = 64;
 constexpr int64_t kMaxDecodeRowsStage = 4096 / 4 * 4;  // rows * MT floats staged per WG <= 16 KB
+constexpr int64_t kDecodeMaxM = 64;         // larger M goes to the tiled kernel
 
 rg_launch_t g_launch = {};                  // all zero: planner defaults
 thread_local int t_last_hip = 0;            // last hipError_t seen by this thread's calls
@@ -64,6 +65,7 @@ struct Plan {
     int64_t Q = 0;
     int max_rows_wg = 0;
     bool x_streamed = false;
+    int mslices = 1;
     int tile_m = 0, tile_n = 0;
 };
 
@@ -133,16 +135,21 @@ bool decode_schedule(int64_t N, int64_t J, int mt, bool x_streamed, const rg_lau
 int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& o, Plan* p) {
     const int64_t J = ceil_div(K, rg::kChunk);
     int want = RG_KERNEL_GENERIC;
-    const int mt = M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 0;
-    const bool decode_ok = fast_ok && mt > 0 && J <= 112;
-    if (decode_ok) want = (mt == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;
+    // decode kernels take x in slices of mt <= 4 rows (several slices for M > 4)
+    const int mt = M <= 1 ? 1 : M <= 2 ? 2 : 4;
+    const int64_t mslices = ceil_div(M, mt);
+    const bool decode_ok = fast_ok && J <= 112 && mslices <= 65536;
+    const bool tiled_ok = fast_ok;
+    if (decode_ok && M <= kDecodeMaxM) want = (M == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;
+    else if (tiled_ok) want = RG_KERNEL_TILED;
     const bool forced = o.kernel > 0;
     if (forced) {
         want = o.kernel - 1;
         if ((want == RG_KERNEL_DECODE || want == RG_KERNEL_DECODE_XS) && !decode_ok) return RG_ERR_RANGE;
-        if (want == RG_KERNEL_DECODE_XS && mt != 1) return RG_ERR_RANGE;
-        if (want == RG_KERNEL_TILED) return RG_ERR_RANGE;  // not built yet
+        if (want == RG_KERNEL_DECODE_XS && M != 1) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_TILED && !tiled_ok) return RG_ERR_RANGE;
     }
+    p->mslices = 1;
     p->kernel = want;
     p->reverse = o.grid_order;
     if (want == RG_KERNEL_DECODE_XS) {
@@ -157,10 +164,24 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     }
     if (want == RG_KERNEL_DECODE) {
         p->mt = mt;
+        p->mslices = (int)mslices;
         if (!decode_schedule(N, J, mt, false, o, p)) {
             if (forced || o.waves_per_wg > 0 || o.grid_wgs > 0 || o.depth > 0) return RG_ERR_RANGE;
-            p->kernel = RG_KERNEL_GENERIC;
+            p->kernel = tiled_ok ? RG_KERNEL_TILED : RG_KERNEL_GENERIC;
+            p->mslices = 1;
         }
+    }
+    if (p->kernel == RG_KERNEL_TILED) {
+        // largest tile that still gives every CU a few workgroups
+        const int64_t t128 = ceil_div(M, 128) * ceil_div(N, 128);
+        const int64_t t64x128 = ceil_div(M, 64) * ceil_div(N, 128);
+        if (t128 >= 2 * kNominalCUs) { p->tile_m = 128; p->tile_n = 128; }
+        else if (t64x128 >= kNominalCUs) { p->tile_m = 64; p->tile_n = 128; }
+        else { p->tile_m = 64; p->tile_n = 64; }
+        const int64_t tiles = ceil_div(M, p->tile_m) * ceil_div(N, p->tile_n);
+        if (tiles > 0x7fffffff) return RG_ERR_RANGE;
+        p->grid = (int)tiles;
+        p->nw = 4;
     }
     if (p->kernel == RG_KERNEL_GENERIC) {
         const int64_t blocks = ceil_div(M * N, 256);
@@ -279,8 +300,15 @@ int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N,
         a.RQ = p.rq;
         a.reverse = p.reverse;
         a.max_rows_wg = p.max_rows_wg;
+        a.groups = p.grid;
+        a.mslices = p.mslices;
+        // decode_kernel: ceil(groups / 8) * 8 * mslices workgroups (the padding ones exit at once)
+        const int64_t blocks = ceil_div(p.grid, 8) * 8 * p.mslices;
+        if (!p.x_streamed && blocks > 0x7fffffff) return RG_ERR_RANGE;
         e = p.x_streamed ? rg::launch_decode1(a, p.grid, p.nw, p.depth, st)
-                         : rg::launch_decode(a, p.mt, p.grid, p.nw, p.depth, st);
+                         : rg::launch_decode(a, p.mt, (int)blocks, p.nw, p.depth, st);
+    } else if (p.kernel == RG_KERNEL_TILED) {
+        e = rg::launch_tiled(x, w, y, M, N, K, p.tile_m, p.tile_n, p.reverse, st);
     } else {
         e = rg::launch_generic(x, w, y, M, N, K, p.grid, p.reverse, st);
     }

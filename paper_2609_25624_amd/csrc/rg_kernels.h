@@ -18,7 +18,9 @@ struct DecodeArgs {
     int J;              // segments: ceil(K / 256)
     uint32_t jmagic;    // ceil(2^32 / J) for J > 1: n / J = umulhi(n, jmagic) for n < 2^16
     int RQ;             // quads per round
-    int reverse;        // 1: workgroup b takes the quads of workgroup grid-1-b
+    int reverse;        // 1: row group g takes the quads of row group groups-1-g
+    int groups;         // row groups (workgroups per slice)
+    int mslices;        // slices of MT rows of x (decode_kernel only; 1 otherwise)
     int max_rows_wg;    // 4 * ceil(Q / grid): rows staged per workgroup
 };
 
@@ -26,6 +28,8 @@ hipError_t launch_generic(const float* x, const uint16_t* w, float* y, int64_t M
                           int grid, int reverse, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipStream_t stream);
+hipError_t launch_tiled(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
+                        int reverse, hipStream_t stream);
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream);
 hipError_t launch_argmax(const float* y, int64_t* out, int64_t M, int64_t N, hipStream_t stream);
 

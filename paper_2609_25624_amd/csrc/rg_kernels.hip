@@ -235,8 +235,22 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     const int RQ = a.RQ;
     const int64_t N = a.N, K = a.K;
 
-    // balanced split of the Q quads over the grid (the first qrem workgroups take one more)
-    const int g = a.reverse ? (int)(gridDim.x - 1 - blockIdx.x) : (int)blockIdx.x;
+    // Row groups g (a.groups of them) x row slices of x (MT rows each).  The
+    // slices of one row group sit 8 workgroups apart, so they are dispatched
+    // to the same XCD at about the same time and share its L2 for W.
+    int g, slice;
+    {
+        const int b = (int)blockIdx.x;
+        const int S = a.mslices;
+        slice = (b >> 3) % S;
+        g = ((b >> 3) / S) * 8 + (b & 7);
+        if (g >= a.groups) return;                         // padding workgroup: no work
+        if (a.reverse) g = a.groups - 1 - g;
+    }
+    const float* xg = a.x + (int64_t)slice * MT * K;       // this slice's rows of x
+    float* yg = a.y + (int64_t)slice * MT * N;
+    const int64_t Ms = a.M - (int64_t)slice * MT;           // rows of x in this slice (>= 1)
+    // balanced split of the Q quads over the row groups (the first qrem take one more)
     const int64_t q0 = (int64_t)g * a.qbase + min(g, a.qrem);
     const int nq = (int)a.qbase + (g < a.qrem ? 1 : 0);
     const int rounds = (nq + RQ - 1) / RQ;
@@ -265,8 +279,8 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 // unconditional load from a clamped address, then zero what is outside x
-                const bool ok = role && m < a.M && kb + 4 * c + 4 <= K;
-                const float4 v = *reinterpret_cast<const float4*>(a.x + (ok ? (int64_t)m * K + kb + 4 * c : 0));
+                const bool ok = role && m < Ms && kb + 4 * c + 4 <= K;
+                const float4 v = *reinterpret_cast<const float4*>(xg + (ok ? (int64_t)m * K + kb + 4 * c : 0));
                 X[m][s][4 * c + 0] = ok ? v.x : 0.0f;
                 X[m][s][4 * c + 1] = ok ? v.y : 0.0f;
                 X[m][s][4 * c + 2] = ok ? v.z : 0.0f;
@@ -392,7 +406,7 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     for (int o = tid; o < rows_wg * MT; o += kThreads) {
         const int m = o / rows_wg, rl = o % rows_wg;
         const int64_t n = rowbase + rl;
-        if (m < a.M && n < N) a.y[(int64_t)m * N + n] = yres[rl * MT + m];
+        if (m < Ms && n < N) yg[(int64_t)m * N + n] = yres[rl * MT + m];
     }
 }
 
@@ -624,6 +638,173 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// tiled kernel (large M): register-tiled SGEMM-shaped kernel, whole K per
+// workgroup, same order.
+//
+// A 256-thread workgroup owns a BM x BN output tile (16 x 16 threads, each
+// holding TM x TN outputs, as two interleaved halves per dimension so that
+// LDS reads are conflict free).  K advances in slabs of 16: x[BM][16] and
+// up(W)[BN][16] are staged transposed in LDS (double buffered, the next slab
+// prefetched into registers while the current one is multiplied).  Each
+// output keeps two registers: the running chain of the current 256-wide
+// segment (from +0, ascending k) and the fold of the finished segments
+// (first segment taken as is, later ones added in ascending order).
+// ---------------------------------------------------------------------------
+constexpr int kTK = 16;   // k per slab
+
+// n consecutive floats from LDS (n = 2, 4 or 8; the address is n*4-byte aligned)
+template <int n>
+__device__ __forceinline__ void lds_vec(const float* p, float* out) {
+    if constexpr (n == 2) {
+        const float2 v = *reinterpret_cast<const float2*>(p);
+        out[0] = v.x; out[1] = v.y;
+    } else {
+        static_assert(n % 4 == 0, "vector width");
+#pragma unroll
+        for (int q = 0; q < n; q += 4) {
+            const float4 v = *reinterpret_cast<const float4*>(p + q);
+            out[q] = v.x; out[q + 1] = v.y; out[q + 2] = v.z; out[q + 3] = v.w;
+        }
+    }
+}
+
+template <int BM, int BN>
+__global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w,
+                                                    float* __restrict__ y, int64_t M, int64_t N, int64_t K,
+                                                    int reverse) {
+    constexpr int TM = BM / 16, TN = BN / 16;        // per-thread outputs per dimension
+    constexpr int HM = TM / 2, HN = TN / 2;          // two interleaved halves
+    static_assert(TM % 2 == 0 && TN % 2 == 0, "tile");
+    constexpr int PADM = BM + 4, PADN = BN + 4;
+    __shared__ __attribute__((aligned(16))) float xs[2][kTK][PADM];
+    __shared__ __attribute__((aligned(16))) float ws[2][kTK][PADN];
+
+    const int tid = threadIdx.x;
+    const int tn = tid & 15, tm = tid >> 4;
+    const int64_t tiles_n = (N + BN - 1) / BN;
+    const int64_t b = reverse ? (int64_t)(gridDim.x - 1 - blockIdx.x) : (int64_t)blockIdx.x;
+    const int64_t m0 = (b / tiles_n) * BM, n0 = (b % tiles_n) * BN;
+
+    // staging roles: x tile BM x 16 floats, W tile BN x 16 bf16
+    constexpr int XF4 = BM * kTK / 4 / 256;          // float4 loads per thread for x
+    constexpr int WU4 = (BN * kTK / 8 + 255) / 256;  // uint4 (8 bf16) loads per thread for W
+    float4 xr[XF4];
+    uint4 wr[WU4];
+
+    auto load_slab = [&](int64_t k0) {
+#pragma unroll
+        for (int u = 0; u < XF4; ++u) {
+            const int idx = tid + 256 * u;            // over BM rows x 4 float4
+            const int row = idx >> 2, kq = idx & 3;
+            const int64_t gm = m0 + row, gk = k0 + 4 * kq;
+            const bool ok = gm < M && gk + 4 <= K;
+            xr[u] = ok ? *reinterpret_cast<const float4*>(x + gm * K + gk) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < WU4; ++u) {
+            const int idx = tid + 256 * u;            // over BN rows x 2 uint4
+            const int row = idx >> 1, kh = idx & 1;
+            const int64_t gn = n0 + row, gk = k0 + 8 * kh;
+            const bool ok = row < BN && gn < N && gk + 8 <= K;
+            wr[u] = ok ? *reinterpret_cast<const uint4*>(w + gn * K + gk) : make_uint4(0u, 0u, 0u, 0u);
+        }
+    };
+    auto store_slab = [&](int buf) {
+#pragma unroll
+        for (int u = 0; u < XF4; ++u) {
+            const int idx = tid + 256 * u;
+            const int row = idx >> 2, kq = idx & 3;
+            xs[buf][4 * kq + 0][row] = xr[u].x;
+            xs[buf][4 * kq + 1][row] = xr[u].y;
+            xs[buf][4 * kq + 2][row] = xr[u].z;
+            xs[buf][4 * kq + 3][row] = xr[u].w;
+        }
+#pragma unroll
+        for (int u = 0; u < WU4; ++u) {
+            const int idx = tid + 256 * u;
+            const int row = idx >> 1, kh = idx & 1;
+            if (row < BN) {
+                const uint32_t d[4] = {wr[u].x, wr[u].y, wr[u].z, wr[u].w};
+#pragma unroll
+                for (int h = 0; h < 8; ++h) ws[buf][8 * kh + h][row] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+            }
+        }
+    };
+
+    float acc[TM][TN], tot[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = 0.0f, tot[i][j] = 0.0f;
+
+    const int64_t nslabs = (K + kTK - 1) / kTK;
+    load_slab(0);
+    store_slab(0);
+    __syncthreads();
+    for (int64_t sl = 0; sl < nslabs; ++sl) {
+        const int buf = (int)(sl & 1);
+        if (sl + 1 < nslabs) load_slab((sl + 1) * kTK);
+        const int kvalid = (int)min((int64_t)kTK, K - sl * kTK);
+        if (kvalid == kTK) {
+#pragma unroll
+            for (int kk = 0; kk < kTK; ++kk) {
+                float xv[TM], wv[TN];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    lds_vec<HM>(&xs[buf][kk][h * (BM / 2) + tm * HM], &xv[h * HM]);
+                    lds_vec<HN>(&ws[buf][kk][h * (BN / 2) + tn * HN], &wv[h * HN]);
+                }
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_fmaf(xv[i], wv[j], acc[i][j]);
+            }
+        } else {
+            for (int kk = 0; kk < kvalid; ++kk) {
+                float xv[TM], wv[TN];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+#pragma unroll
+                    for (int q = 0; q < HM; ++q) xv[h * HM + q] = xs[buf][kk][h * (BM / 2) + tm * HM + q];
+#pragma unroll
+                    for (int q = 0; q < HN; ++q) wv[h * HN + q] = ws[buf][kk][h * (BN / 2) + tn * HN + q];
+                }
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_fmaf(xv[i], wv[j], acc[i][j]);
+            }
+        }
+        // end of a 256-wide segment (or of K): fold the segment chain, restart it from +0
+        const int64_t kend = sl * kTK + kvalid;
+        if ((kend % kChunk) == 0 || kend == K) {
+            const bool first = kend <= kChunk;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    tot[i][j] = first ? acc[i][j] : tot[i][j] + acc[i][j];
+                    acc[i][j] = 0.0f;
+                }
+        }
+        if (sl + 1 < nslabs) {
+            store_slab(buf ^ 1);
+            __syncthreads();
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int64_t gm = m0 + (i < HM ? tm * HM + i : BM / 2 + tm * HM + (i - HM));
+        if (gm >= M) continue;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int64_t gn = n0 + (j < HN ? tn * HN + j : BN / 2 + tn * HN + (j - HN));
+            if (gn < N) y[gm * N + gn] = tot[i][j];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // cast kernel (comparison point only: the transient FP32 weight copy)
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) cast_kernel(const uint16_t* __restrict__ w, float* __restrict__ o,
@@ -745,6 +926,18 @@ hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int dept
         case 4: return launch_decode_w<4>(a, grid, nw, depth, stream);
         default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_tiled(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
+                        int reverse, hipStream_t stream) {
+    const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+    if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)tiles), block(256);
+    if (bm == 128 && bn == 128) hipLaunchKernelGGL((tiled_kernel<128, 128>), grid, block, 0, stream, x, w, y, M, N, K, reverse);
+    else if (bm == 64 && bn == 128) hipLaunchKernelGGL((tiled_kernel<64, 128>), grid, block, 0, stream, x, w, y, M, N, K, reverse);
+    else if (bm == 64 && bn == 64) hipLaunchKernelGGL((tiled_kernel<64, 64>), grid, block, 0, stream, x, w, y, M, N, K, reverse);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
 }
 
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream) {

@@ -60,6 +60,9 @@ def test_plan_kernel_choice():
     assert rg.rg_plan(1, 8192, 28672)["kernel_name"] == "decode"     # J = 112 needs 7 waves
     assert rg.rg_plan(4, 6144, 4096)["kernel_name"] == "decode"
     assert rg.rg_plan(1, 10, 7)["kernel_name"] == "generic"     # K % 8 != 0
+    assert rg.rg_plan(16, 6144, 4096)["kernel_name"] == "decode"  # 4 slices of 4 rows
+    assert rg.rg_plan(65, 6144, 4096)["kernel_name"] == "tiled"
+    assert rg.rg_plan(2048, 57344, 8192)["kernel_name"] == "tiled"
 
 
 def test_set_launch_range_checks():

@@ -163,9 +163,16 @@ def test_config5_70b_m1(name, N, K):
 @pytest.mark.parametrize("name,N,K", [("70b_gate_up", 57344, 8192), ("70b_down", 8192, 28672)])
 def test_config5_70b_m2048_sampled(name, N, K):
     import paper_2609_25624_amd as rg
-    if rg.rg_plan(2048, N, K)["kernel_name"] == "generic":
-        pytest.skip("prefill-size shape routes to the one-thread-per-output kernel; too slow at this size")
+    assert rg.rg_plan(2048, N, K)["kernel_name"] == "tiled"
     _check_layer(2048, N, K, w_std=0.01, layer_id=9, sampled=4000)
+
+
+@pytest.mark.parametrize("M,N,K", [(65, 130, 1000), (100, 1000, 1000), (128, 256, 4096), (129, 257, 264),
+                                   (300, 77, 520), (256, 4096, 4096), (2048, 192, 8200)])
+def test_tiled_shapes(M, N, K):
+    import paper_2609_25624_amd as rg
+    assert rg.rg_plan(M, N, K)["kernel_name"] == "tiled"
+    _check_layer(M, N, K, seed=M + K)
 
 
 @pytest.mark.parametrize("M", [1, 2, 3, 4, 5, 9])
@@ -226,12 +233,15 @@ def _launch_settings():
         dict(kernel="decode", waves_per_wg=7, grid_wgs=300),
         dict(kernel="decode_xs", waves_per_wg=6),
         dict(kernel="decode_xs", waves_per_wg=2, depth=3, grid_wgs=1000, grid_order=1),
+        dict(kernel="tiled"),
+        dict(kernel="tiled", grid_order=1),
         dict(kernel="generic"),
         dict(kernel="generic", grid_wgs=3, grid_order=1),
     ]
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 6144, 4096), (1, 4096, 14336), (3, 1000, 1000), (4, 2048, 2560)])
+@pytest.mark.parametrize("M,N,K", [(1, 6144, 4096), (1, 4096, 14336), (3, 1000, 1000), (4, 2048, 2560),
+                                   (16, 2048, 4096), (70, 1024, 1024)])
 def test_launch_settings_do_not_change_bits(M, N, K):
     import torch
     import paper_2609_25624_amd as rg
