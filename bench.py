@@ -39,11 +39,213 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-baseline-scheme", action="store_true")
+    ap.add_argument("--configs", action="store_true",
+                    help="instead of the one-line step benchmark, time every config (M=1 8B layers, M=4/16/64, "
+                         "LM head M=1/16, 70B layers at M=1 and M=2048) and print one JSON line each")
+    ap.add_argument("--trace-summary", metavar="KERNEL_TRACE_CSV",
+                    help="summarise a rocprofv3 --kernel-trace CSV of a run of this script made with the same "
+                         "--steps/--warmup/--per-layer-calls (no GPU needed) and exit")
+    ap.add_argument("--counter-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise the rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE CSVs of two --profile-kernels "
+                         "runs into HBM bytes per gate+up launch (no GPU needed) and exit")
+    ap.add_argument("--profile-kernels", action="store_true",
+                    help="short run for hardware counters: 20 launches of the gate+up M=1 layer, then 5 plain "
+                         "device copies of 256 MiB (the calibration kernel for HBM byte counters)")
     return ap.parse_args()
+
+
+def profile_kernels():
+    """Dispatches for rocprofv3 counter runs: the dominant kernel, then a copy of known size."""
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2609_25624_amd as rg
+    dev = torch.device("cuda:0")
+    N, K = 28672, 4096
+    x, w = synth.layer_inputs(1, N, K, seed=0, w_std=0.02, layer=2)
+    xd = torch.from_numpy(x).to(dev)
+    ws = [torch.from_numpy(w.view(np.int16)).to(dev)]
+    ws += [ws[0].clone() for _ in range(2)]
+    y = torch.empty((1, N), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    for i in range(20):
+        rg.rg_linear(xd, ws[i % 3], y)
+    torch.cuda.synchronize()
+    src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    dst = [torch.empty_like(src) for _ in range(2)]
+    src.fill_(1)
+    torch.cuda.synchronize()
+    for i in range(5):
+        dst[i % 2].copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"profiled": "gate_up decode x20, copy 256MiB x5", "copy_bytes": 256 << 20,
+                      "decode_algorithmic_bytes": 2 * N * K + 4 * K + 4 * N}), flush=True)
+
+
+CONFIGS = [
+    # (config, name, M, N, K, w_std)
+    (1, "small_1024", 1, 1024, 1024, 0.02),
+    (2, "qkv", 1, 6144, 4096, 0.02), (2, "o", 1, 4096, 4096, 0.02),
+    (2, "gate_up", 1, 28672, 4096, 0.02), (2, "down", 1, 4096, 14336, 0.02),
+    (3, "qkv", 4, 6144, 4096, 0.02), (3, "o", 4, 4096, 4096, 0.02),
+    (3, "gate_up", 4, 28672, 4096, 0.02), (3, "down", 4, 4096, 14336, 0.02),
+    (3, "qkv", 16, 6144, 4096, 0.02), (3, "o", 16, 4096, 4096, 0.02),
+    (3, "gate_up", 16, 28672, 4096, 0.02), (3, "down", 16, 4096, 14336, 0.02),
+    (3, "qkv", 64, 6144, 4096, 0.02), (3, "o", 64, 4096, 4096, 0.02),
+    (3, "gate_up", 64, 28672, 4096, 0.02), (3, "down", 64, 4096, 14336, 0.02),
+    (4, "lm_head", 1, 128256, 4096, 0.02), (4, "lm_head", 16, 128256, 4096, 0.02),
+    (5, "70b_gate_up", 1, 57344, 8192, 0.01), (5, "70b_down", 1, 8192, 28672, 0.01),
+    (5, "70b_gate_up", 2048, 57344, 8192, 0.01), (5, "70b_down", 2048, 8192, 28672, 0.01),
+]
+FP32_VECTOR_PEAK_TFLOPS = 157.3      # vendor figure (packed FP32)
+FP32_UNPACKED_PEAK_TFLOPS = 78.6     # without packed FP32 instructions (not used by these kernels)
+
+
+def run_configs():
+    import numpy as np
+    import torch
+
+    import oracle
+    import synth
+    import paper_2609_25624_amd as rg
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    for cfg, name, M, N, K, std in CONFIGS:
+        x, w = synth.layer_inputs(M, N, K, seed=0, w_std=std, layer=hash(name) % 97)
+        xd = torch.from_numpy(x).to(dev)
+        w0 = torch.from_numpy(w.view(np.int16)).to(dev)
+        nrot = max(1, int(np.ceil(ROTATE_BYTES / (2.0 * N * K))))
+        ws = [w0] + [w0.clone() for _ in range(nrot - 1)]
+        y = torch.empty((M, N), dtype=torch.float32, device=dev)
+        flops = 2.0 * M * N * K
+        R = int(min(200, max(3, 2e10 / max(flops, 1.0))))
+        for i in range(min(R, 5)):
+            rg.rg_linear(xd, ws[i % nrot], y, stream=stream)
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for i in range(R):
+            rg.rg_linear(xd, ws[i % nrot], y, stream=stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) * 1e3 / R
+        rg.rg_linear(xd, ws[0], y, stream=stream)
+        torch.cuda.synchronize()
+        got = y.cpu().numpy()
+        if M * N * K <= 1.5e10:
+            want = oracle.linear(x, w)
+            exact = bool(np.array_equal(got.view(np.uint32), want.view(np.uint32)))
+            checked = "all"
+        else:
+            rng = np.random.default_rng(1)
+            rows, cols = rng.integers(0, M, 4096), rng.integers(0, N, 4096)
+            want = oracle.linear_sampled(x, w, rows, cols)
+            exact = bool(np.array_equal(got[rows, cols].view(np.uint32), want.view(np.uint32)))
+            checked = "4096 sampled"
+        plan = rg.rg_plan(M, N, K)
+        tflops = flops / (us * 1e-6) / 1e12
+        print(json.dumps({
+            "config": cfg, "layer": name, "M": M, "N": N, "K": K, "us_per_call": round(us, 3),
+            "weight_TBs": round(2.0 * N * K / (us * 1e-6) / 1e12, 4),
+            "frac_of_8TBs": round(2.0 * N * K / (us * 1e-6) / (HBM_PEAK_GBS * 1e9), 4),
+            "TFLOPs": round(tflops, 3), "frac_of_fp32_157": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
+            "frac_of_fp32_unpacked_78.6": round(tflops / FP32_UNPACKED_PEAK_TFLOPS, 4),
+            "bitexact": exact, "checked": checked, "kernel": plan["kernel_name"], "calls_timed": R,
+            "rotated_copies": nrot}), flush=True)
+        del xd, ws, w0, y
+        torch.cuda.empty_cache()
+
+
+def _csv_rows(path):
+    import csv
+    rows = list(csv.DictReader(open(path)))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return rows
+
+
+def trace_summary(path, args):
+    """Per-layer kernel durations from a rocprofv3 kernel trace of this script.
+
+    The library's dispatches come in a fixed order: warmup and timed steps
+    (four layers each), then per layer 10 untimed and --per-layer-calls timed
+    calls, then one call per layer for the exactness check.  The durations of
+    each layer's timed block are the ones the per-layer event timing reports."""
+    rows = [r for r in _csv_rows(path) if "rg::decode" in r["Kernel_Name"] or "rg::tiled" in r["Kernel_Name"]
+            or "rg::generic" in r["Kernel_Name"]]
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    i = (args.warmup + args.steps) * len(LAYERS)
+    lines = [f"dispatches of the library's linear kernels: {len(rows)}",
+             f"{'layer':8s} {'kernel':40s} {'calls':>5s} {'avg_us':>8s} {'min_us':>8s} {'max_us':>8s} {'TB/s':>6s}"]
+    for name, N, K in LAYERS:
+        blk = rows[i + 10:i + 10 + args.per_layer_calls]
+        i += 10 + args.per_layer_calls
+        d = [dur(r) for r in blk]
+        avg = sum(d) / len(d)
+        lines.append(f"{name:8s} {blk[0]['Kernel_Name'][:40]:40s} {len(d):5d} {avg:8.3f} {min(d):8.3f} {max(d):8.3f} "
+                     f"{2.0 * N * K / (avg * 1e-6) / 1e12:6.3f}")
+    st = rows[args.warmup * len(LAYERS):(args.warmup + args.steps) * len(LAYERS)]
+    tot = sum(dur(r) for r in st) / args.steps
+    lines.append(f"timed steps: sum of the four kernel durations per step {tot:.3f} us")
+    print("\n".join(lines))
+
+
+def counter_summary(fetch_csv, write_csv):
+    """HBM bytes per gate+up launch from FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each scaled by the
+    reading of the same counter for a 256 MiB device-to-device copy (reads and writes 256 MiB)."""
+    copy_kib = 256 * 1024
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = [r for r in _csv_rows(path) if r["Counter_Name"] == counter]
+        dec = [float(r["Counter_Value"]) for r in rows if "rg::decode" in r["Kernel_Name"]]
+        cp = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]
+              and abs(float(r["Counter_Value"]) - copy_kib) < 0.6 * copy_kib]
+        cp_avg = sum(cp[-5:]) / len(cp[-5:])
+        factor = copy_kib / cp_avg
+        out[counter] = dict(kernel_kib=sum(dec) / len(dec), dispatches=len(dec), copy_kib=cp_avg, factor=factor,
+                            bytes=sum(dec) / len(dec) * factor * 1024)
+    N, K = 28672, 4096
+    algo = 2 * N * K + 4 * K + 4 * N
+    total = out["FETCH_SIZE"]["bytes"] + out["WRITE_SIZE"]["bytes"]
+    lines = []
+    for c, v in out.items():
+        lines.append(f"{c}: gate+up decode {v['kernel_kib']:.2f} KiB/dispatch over {v['dispatches']} dispatches; "
+                     f"256 MiB copy reads {v['copy_kib']:.2f} KiB -> factor {v['factor']:.5f}; "
+                     f"scaled {v['bytes']:.0f} B")
+    lines.append(f"algorithmic_bytes_per_launch = {algo}")
+    lines.append(f"bytes_per_launch = {total:.0f}")
+    lines.append(f"traffic_over_algorithmic = {total / algo:.5f}")
+    lines.append(f"kernel_source_hash = {_kernel_hash()}")
+    print("\n".join(lines))
+
+
+def _read_traffic():
+    """bytes_per_launch from the committed counter summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "decode_gate_up_m1_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if " = " in line:
+            k, v = line.split(" = ", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_hash") != _kernel_hash():
+        return None
+    try:
+        return int(float(kv["bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
 
 
 def main():
     args = parse()
+    if args.trace_summary:
+        trace_summary(args.trace_summary, args)
+        return
+    if args.counter_summary:
+        counter_summary(*args.counter_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
@@ -60,6 +262,12 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     torch.backends.cuda.matmul.allow_tf32 = False
+    if args.profile_kernels:
+        profile_kernels()
+        return
+    if args.configs:
+        run_configs()
+        return
     stream = torch.cuda.current_stream()
 
     # ---- inputs: seeded on the host, copied once, rotated copies made on the device ----
@@ -131,15 +339,7 @@ def main():
     dom = next(L for L in layers if L["name"] == "gate_up")
     dom_us = per_layer["gate_up"]["us_per_call"]
     achieved = dom["algo_bytes"] / (dom_us * 1e-6) / 1e9
-    traffic = None
-    tfile = os.path.join(ROOT, "profiles", "decode_gate_up_m1_traffic.json")
-    if os.path.exists(tfile):
-        try:
-            t = json.load(open(tfile))
-            if t.get("kernel_source_hash") == _kernel_hash():
-                traffic = t.get("bytes_per_launch")
-        except Exception:
-            traffic = None
+    traffic = _read_traffic()
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
                     kernel=f"decode (gate+up 28672x4096, M=1, {dom['plan']['waves_per_wg']} waves/WG)",
@@ -184,7 +384,7 @@ def main():
                 oracle.linear(L["x"], L["w"], nthreads=threads)
             reps += 1
             el = time.perf_counter() - t_start
-            if el >= args.cpu_seconds or reps >= 200:
+            if el >= args.cpu_seconds or reps >= 5000:
                 break
         cpu = dict(value=round(reps * step_wbytes / el / 1e12, 6), unit="TB/s", cores=threads, kind="oracle",
                    sample=f"{reps} full steps (4 layers, M=1) in {el:.1f} s")
