@@ -70,7 +70,8 @@ typedef enum {
     RG_KERNEL_GENERIC = 0,   /* one thread per output; any K, any alignment */
     RG_KERNEL_DECODE = 1,    /* M <= 4: streaming GEMV / skinny GEMM, x in registers */
     RG_KERNEL_TILED = 2,     /* larger M: register-tiled kernel, whole K per workgroup */
-    RG_KERNEL_DECODE_XS = 3  /* M == 1: streaming GEMV with x streamed through LDS beside W */
+    RG_KERNEL_DECODE_XS = 3, /* M == 1: streaming GEMV with x streamed through LDS beside W */
+    RG_KERNEL_GEMV = 4       /* M == 1, K % 256 == 0, K >= 4096: 32 KB W bursts, whole rows per wave */
 } rg_kernel_id;
 
 /* Scheduling overrides for the determinism tests.  0 in a field = planner
@@ -79,9 +80,10 @@ typedef enum {
  *   kernel        : -1/0 = planner's choice, else 1 + rg_kernel_id to force one
  *                   (a kernel that cannot handle the shape is not forced; the
  *                    call returns RG_ERR_RANGE)
- *   waves_per_wg  : 1..8  waves (64 threads each) per workgroup
+ *   waves_per_wg  : 1..8  waves (64 threads each) per workgroup (gemv: 1..4, fewer
+ *                   when x must fit in LDS beside the slots)
  *   grid_wgs      : 1..65536 workgroups (work is spread over them evenly)
- *   depth         : 2..3  decode pipeline depth in 128-byte-per-row slabs
+ *   depth         : 2..3  decode pipeline depth in 128-byte-per-row slabs (unused by gemv)
  *   grid_order    : 0 = forward, 1 = reversed workgroup-to-rows mapping
  */
 typedef struct {

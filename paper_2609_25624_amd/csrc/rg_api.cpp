@@ -131,6 +131,57 @@ bool decode_schedule(int64_t N, int64_t J, int mt, bool x_streamed, const rg_lau
     return true;
 }
 
+// Dense-stream M == 1 kernel: K a multiple of 256 with J >= 16 segments (64
+// lanes of a wave = 4 rows x 16 segments).  LDS per workgroup: a 32 KB slot
+// and 256 bytes of partials per wave, plus all of x (4K bytes).
+constexpr int64_t kLdsBytes = 160 * 1024 - 1024;
+constexpr int kGemvWaveLds = 32768 + 256;
+
+int gemv_max_waves(int64_t K) {
+    const int64_t nw = (kLdsBytes - 4 * K) / kGemvWaveLds;
+    return nw < 0 ? 0 : (nw > 4 ? 4 : (int)nw);
+}
+
+bool gemv_shape_ok(int64_t N, int64_t K) {
+    return K % rg::kChunk == 0 && K / rg::kChunk >= 16 && K <= ((int64_t)1 << 26) &&
+           ceil_div(N, 4) < ((int64_t)1 << 31) && gemv_max_waves(K) >= 2;
+}
+
+// Waves and workgroups of the dense stream.  Default: the fewest rounds of
+// quads per wave that 256 workgroups of up to nwmax waves allow, then as few
+// waves as give that many rounds (every wave the same number of quads when
+// the shape allows), spread over as many workgroups as possible.
+bool gemv_schedule(int64_t N, int64_t K, const rg_launch_t& o, Plan* p) {
+    const int nwmax = gemv_max_waves(K);
+    const int64_t Q = ceil_div(N, 4);
+    int nw = 0;
+    int64_t G = 0;
+    if (o.waves_per_wg > 0) {
+        if (o.waves_per_wg > nwmax) return false;
+        nw = o.waves_per_wg;
+    }
+    if (o.grid_wgs > 0) G = o.grid_wgs;
+    if (nw == 0 && G == 0) {
+        const int64_t rounds = ceil_div(Q, (int64_t)kNominalCUs * nwmax);
+        const int64_t vneed = ceil_div(Q, rounds);
+        nw = (int)ceil_div(vneed, kNominalCUs);
+        G = ceil_div(vneed, nw);
+    } else if (nw == 0) {
+        nw = (int)ceil_div(Q, G);
+        if (nw > nwmax) nw = nwmax;
+        if (nw < 1) nw = 1;
+    } else if (G == 0) {
+        G = ceil_div(Q, nw);
+        if (G > kNominalCUs) G = kNominalCUs;
+    }
+    p->nw = nw;
+    p->grid = (int)G;
+    p->Q = Q;
+    p->depth = 0;
+    p->rq = nw;
+    return true;
+}
+
 // The planner.  `fast_ok`: x and W 16-byte aligned and K % 8 == 0.
 int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& o, Plan* p) {
     const int64_t J = ceil_div(K, rg::kChunk);
@@ -140,7 +191,12 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     const int64_t mslices = ceil_div(M, mt);
     const bool decode_ok = fast_ok && J <= 112 && mslices <= 65536;
     const bool tiled_ok = fast_ok;
-    if (decode_ok && M <= kDecodeMaxM) want = (M == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;
+    const bool gemv_ok = fast_ok && M == 1 && gemv_shape_ok(N, K);
+    // M == 1: the 32 KB-burst kernel where one step covers K (J == 16); the
+    // slab-streaming kernels elsewhere (they measure faster once x must be
+    // re-read from LDS every step)
+    if (gemv_ok && ceil_div(K, rg::kChunk) == 16) want = RG_KERNEL_GEMV;
+    else if (decode_ok && M <= kDecodeMaxM) want = (M == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;
     else if (tiled_ok) want = RG_KERNEL_TILED;
     const bool forced = o.kernel > 0;
     if (forced) {
@@ -148,10 +204,16 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         if ((want == RG_KERNEL_DECODE || want == RG_KERNEL_DECODE_XS) && !decode_ok) return RG_ERR_RANGE;
         if (want == RG_KERNEL_DECODE_XS && M != 1) return RG_ERR_RANGE;
         if (want == RG_KERNEL_TILED && !tiled_ok) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_GEMV && !gemv_ok) return RG_ERR_RANGE;
     }
     p->mslices = 1;
     p->kernel = want;
     p->reverse = o.grid_order;
+    if (want == RG_KERNEL_GEMV) {
+        if (gemv_schedule(N, K, o, p)) return RG_OK;
+        if (forced) return RG_ERR_RANGE;
+        want = p->kernel = decode_ok ? RG_KERNEL_DECODE_XS : (tiled_ok ? RG_KERNEL_TILED : RG_KERNEL_GENERIC);
+    }
     if (want == RG_KERNEL_DECODE_XS) {
         // M == 1: x streamed beside W, when its wave counts cover J; else x in registers.
         p->mt = 1;
@@ -194,7 +256,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
 }
 
 int validate_launch(const rg_launch_t& c) {
-    if (c.kernel < -1 || c.kernel > 4) return RG_ERR_RANGE;
+    if (c.kernel < -1 || c.kernel > 5) return RG_ERR_RANGE;
     if (c.waves_per_wg < 0 || c.waves_per_wg > 8) return RG_ERR_RANGE;
     if (c.grid_wgs < 0 || c.grid_wgs > 65536) return RG_ERR_RANGE;
     if (c.depth < 0 || c.depth > 3 || c.depth == 1) return RG_ERR_RANGE;
@@ -284,7 +346,21 @@ int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N,
     hipStream_t st = (hipStream_t)stream;
     (void)hipGetLastError();   // drop an error left by an unrelated earlier HIP call on this thread
     hipError_t e = hipSuccess;
-    if (p.kernel == RG_KERNEL_DECODE || p.kernel == RG_KERNEL_DECODE_XS) {
+    if (p.kernel == RG_KERNEL_GEMV) {
+        rg::GemvArgs a;
+        a.x = x;
+        a.w = w;
+        a.y = y;
+        a.N = N;
+        a.K = K;
+        const int64_t V = (int64_t)p.grid * p.nw;
+        a.qbase = p.Q / V;
+        a.qrem = p.Q % V;
+        a.J = (int)(K / rg::kChunk);
+        a.S = (int)ceil_div(a.J, 16);
+        a.reverse = p.reverse;
+        e = rg::launch_gemv(a, p.grid, p.nw, st);
+    } else if (p.kernel == RG_KERNEL_DECODE || p.kernel == RG_KERNEL_DECODE_XS) {
         rg::DecodeArgs a;
         a.x = x;
         a.w = w;

@@ -24,10 +24,24 @@ struct DecodeArgs {
     int max_rows_wg;    // 4 * ceil(Q / grid): rows staged per workgroup
 };
 
+// Arguments of the M == 1 dense-stream kernel (K % 256 == 0, K >= 4096).
+struct GemvArgs {
+    const float* x;
+    const uint16_t* w;
+    float* y;
+    int64_t N, K;
+    int64_t qbase;      // Q / V quads per wave (Q = ceil(N / 4), V = waves in the grid) ...
+    int64_t qrem;       // ... plus one for waves v < Q % V
+    int J;              // segments: K / 256
+    int S;              // wave steps per quad: ceil(J / 16)
+    int reverse;        // 1: workgroup b takes the quads of workgroup grid-1-b
+};
+
 hipError_t launch_generic(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K,
                           int grid, int reverse, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipStream_t stream);
+hipError_t launch_gemv(const GemvArgs& a, int grid, int nw, hipStream_t stream);
 hipError_t launch_tiled(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
                         int reverse, hipStream_t stream);
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream);

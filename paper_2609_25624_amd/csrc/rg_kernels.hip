@@ -16,6 +16,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "rg_kernels.h"
 
 namespace rg {
@@ -805,6 +807,222 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
 }
 
 // ---------------------------------------------------------------------------
+// gemv kernel (M == 1, K a multiple of 256 with at least 16 segments):
+// dense weight stream.
+//
+// Work split.  W rows are grouped in quads of 4 consecutive rows.  The grid
+// has V waves in all; wave v owns quads v, v + V, v + 2V, ..., so at any
+// moment the whole grid reads one compact window of W, and each wave owns
+// whole rows: every output is finished inside one wave (no cross-wave or
+// cross-workgroup reduction, no atomics, no barriers in the stream).
+//
+// Data path.  A wave step covers segments 16s .. 16s+15 of the quad's 4 rows
+// (4 x 8 KB of W, contiguous within each row).  The wave requests the whole
+// step at once with 32 global->LDS DMA instructions (8 lanes per 128-byte
+// line) into its own 32 KB LDS slot, so each DRAM page of the window is read
+// in one burst.  The DMA image is ordered by quarter: quarter q holds
+// elements 64q .. 64q+63 of every segment, so the step is consumed quarter by
+// quarter as its DMA instructions land (they complete in issue order) and
+// only one quarter's FMAs follow the last byte.  The next step is requested
+// as soon as the slot has been read.  Inside a quarter the 128-byte image of
+// a lane is XOR-swizzled by ((lane >> 1) & 7) in 16-byte units, so the
+// transposing ds_read_b128 are conflict-free.
+//
+// Lane roles.  Lane c = 4j + r owns segment 16s + j of row r of the quad and
+// runs its whole 256-long fmaf chain from +0 inside the step.  The 4 lanes of
+// a DPP quad share a segment; lane r holds x for elements 64r .. 64r+63 of it
+// and the others read those through quad broadcasts fused into v_fmac_f32.
+// x stays in registers when one step covers K (K = 4096); otherwise the
+// workgroup keeps all of x in LDS and each lane reads its 64 values per step.
+//
+// Order.  After a step the 16 segment partials of each row go to LDS and
+// lane r folds them into row r's running sum in ascending segment order
+// (the first partial starts the sum); after the quad's last step lane r
+// stores the row.
+// ---------------------------------------------------------------------------
+constexpr int kGemvSlabBytes = 32768;   // 4 rows x 16 segments x 512 bytes of W
+
+template <int NW, bool XL>
+__global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
+    __shared__ __attribute__((aligned(16))) uint8_t wslot[NW][kGemvSlabBytes];
+    __shared__ __attribute__((aligned(16))) float fold[NW][64];   // [row r][segment j] of the step
+    extern __shared__ __attribute__((aligned(16))) uint8_t ximg[]; // x, K floats, swizzled
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int J = a.J, S = a.S;
+    const int64_t N = a.N, K = a.K;
+    const int g = a.reverse ? (int)(gridDim.x - 1 - blockIdx.x) : (int)blockIdx.x;
+    const int64_t V = (int64_t)gridDim.x * NW;
+    const int64_t v = (int64_t)g * NW + wave;
+    const int nq = (int)a.qbase + (v < a.qrem ? 1 : 0);   // quads of this wave
+    const int64_t row_bytes = 2 * K;
+
+    // ---- DMA roles: instruction 8q + m, this lane fills consumer lane c = 8m + (lane >> 3),
+    // 16-byte slot (lane & 7), which holds piece u = slot ^ ((c >> 1) & 7) of quarter q ----
+    uint32_t doff[8];   // byte offset of quarter 0's piece inside the step window, full step
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+        const int c = 8 * m + (lane >> 3);
+        const int u = (lane & 7) ^ ((c >> 1) & 7);
+        doff[m] = (uint32_t)((c & 3) * row_bytes) + 512u * (uint32_t)(c >> 2) + 16u * (uint32_t)u;
+    }
+    const uint32_t wbase = lds_addr(&wslot[wave][0]);
+
+    // request step (t, s): quad v + t*V, segments 16s .. 16s+15 (32 DMA instructions)
+    auto issue = [&](int t, int s) {
+        const int64_t row0 = 4 * (v + (int64_t)t * V);
+        const char* base = reinterpret_cast<const char*>(a.w) + row0 * row_bytes + (int64_t)s * 8192;
+        if (row0 + 4 <= N && 16 * (s + 1) <= J) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int m = 0; m < 8; ++m) dma16(base, doff[m] + 128u * q, wbase + 1024u * (8 * q + m));
+        } else {
+            // a short last quad or step: absent rows and segments re-read present ones
+            // (the same lines as other lanes of the instruction or an earlier one)
+            const int rlim = (int)(N - 1 - row0);
+            const int jlim = J - 1 - 16 * s;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int m = 0; m < 8; ++m) {
+                    const int c = 8 * m + (lane >> 3);
+                    const int u = (lane & 7) ^ ((c >> 1) & 7);
+                    const int r = min(c & 3, rlim), j = min(c >> 2, jlim);
+                    const uint32_t voff = (uint32_t)(r * row_bytes) + 512u * (uint32_t)j + 16u * (uint32_t)(8 * q + u);
+                    dma16(base, voff, wbase + 1024u * (8 * q + m));
+                }
+        }
+    };
+
+    // ---- x image, fetched by DMA ahead of the first W step and shared by the waves:
+    // 256-byte piece P = x[64P, 64P+64) at LDS 256P, its 16-byte slot i at slot i ^ (P & 15).
+    // Instruction b (1 KB) holds pieces 4b .. 4b+3; the waves take b = wave, wave + NW, ... ----
+    {
+        const uint32_t xbase = lds_addr(ximg);
+        const int nxi = (int)(K >> 8);
+        const int P0 = lane >> 4, sl = lane & 15;
+        int pending = 0;
+        for (int b = wave; b < nxi; b += NW) {
+            if (pending == 31) {      // keep this wave's outstanding operations (x + 32 W) within 63
+                vmcnt_wait<0>();
+                pending = 0;
+            }
+            const int P = 4 * b + P0;
+            dma16(a.x, (uint32_t)(256 * P + 16 * (sl ^ (P & 15))), xbase + 1024u * (uint32_t)b);
+            ++pending;
+        }
+    }
+    if (nq > 0) {
+        issue(0, 0);
+        vmcnt_wait<32>();     // this wave's x instructions (issued first) have landed
+    } else {
+        vmcnt_wait<0>();
+    }
+    __syncthreads();          // the whole x image is in LDS
+
+    // lane c reads x piece P (segment P / 4, part P % 4) into X[0..63]
+    float X[64];
+    auto load_x = [&](int P) {
+        const uint8_t* xp = ximg + 256 * P;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const float4 t4 = *reinterpret_cast<const float4*>(xp + 16 * (i ^ (lane & 15)));
+            X[4 * i + 0] = t4.x;
+            X[4 * i + 1] = t4.y;
+            X[4 * i + 2] = t4.z;
+            X[4 * i + 3] = t4.w;
+        }
+    };
+    if constexpr (!XL) load_x(lane);   // one step covers K: the same x every step
+
+    const int sw = (lane >> 1) & 7;
+    const uint8_t* rd = &wslot[wave][128 * lane];
+    float yrun = 0.0f;   // lanes 0..3: running fold of row `lane` of the current quad
+
+    for (int t = 0; t < nq; ++t) {
+        for (int s = 0; s < S; ++s) {
+            const bool more = (s + 1 < S) || (t + 1 < nq);
+            // x for segment 16s + j, part r: piece P = 64s + lane (present segments only)
+            if constexpr (XL) load_x((16 * s + (lane >> 2) < J) ? 64 * s + lane : lane);
+            float acc = 0.0f;
+            auto chain8 = [&](auto qc, const uint4& p, int u) {
+                constexpr int q = decltype(qc)::value;
+                const uint32_t d[4] = {p.x, p.y, p.z, p.w};
+                float wv[8];
+#pragma unroll
+                for (int h = 0; h < 8; ++h) wv[h] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+                fmac8_bcast<q>(acc, &X[8 * u], wv);
+            };
+            if (more) {
+                // whole step to registers, request the next one into the freed slot, then the chains
+                vmcnt_wait<0>();
+                uint4 wp[32];
+#pragma unroll
+                for (int i = 0; i < 32; ++i)
+                    wp[i] = *reinterpret_cast<const uint4*>(rd + 8192 * (i >> 3) + 16 * ((i & 7) ^ sw));
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                issue(s + 1 < S ? t : t + 1, s + 1 < S ? s + 1 : 0);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 0>{}, wp[u], u);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 1>{}, wp[8 + u], u);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 2>{}, wp[16 + u], u);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 3>{}, wp[24 + u], u);
+            } else {
+                // this wave's last step: consume each quarter as its 8 DMA instructions land
+                // (at most 8 * (3 - q) of the step's instructions outstanding; later
+                // operations only add slack)
+                auto quarter = [&](auto qc) {
+                    constexpr int q = decltype(qc)::value;
+                    vmcnt_wait<8 * (3 - q)>();
+                    uint4 wp[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u)
+                        wp[u] = *reinterpret_cast<const uint4*>(rd + 8192 * q + 16 * (u ^ sw));
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) chain8(qc, wp[u], u);
+                };
+                quarter(std::integral_constant<int, 0>{});
+                quarter(std::integral_constant<int, 1>{});
+                quarter(std::integral_constant<int, 2>{});
+                quarter(std::integral_constant<int, 3>{});
+            }
+
+            // ascending fold of the step's segment partials into each row's sum
+            fold[wave][16 * (lane & 3) + (lane >> 2)] = acc;
+            __builtin_amdgcn_wave_barrier();
+            if (lane < 4) {
+                float p[16];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float4 t4 = *reinterpret_cast<const float4*>(&fold[wave][16 * lane + 4 * i]);
+                    p[4 * i + 0] = t4.x;
+                    p[4 * i + 1] = t4.y;
+                    p[4 * i + 2] = t4.z;
+                    p[4 * i + 3] = t4.w;
+                }
+                const int jn = min(16, J - 16 * s);
+                float y = (s == 0) ? p[0] : yrun + p[0];
+#pragma unroll
+                for (int i = 1; i < 16; ++i)
+                    if (i < jn) y = y + p[i];
+                yrun = y;
+                if (s == S - 1) {
+                    const int64_t n = 4 * (v + (int64_t)t * V) + lane;
+                    if (n < N) a.y[n] = y;
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // cast kernel (comparison point only: the transient FP32 weight copy)
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) cast_kernel(const uint16_t* __restrict__ w, float* __restrict__ o,
@@ -915,6 +1133,30 @@ hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipS
         case 42: return launch_decode1_t<4, 2>(a, grid, stream);
         case 43: return launch_decode1_t<4, 3>(a, grid, stream);
         case 62: return launch_decode1_t<6, 2>(a, grid, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <int NW, bool XL>
+static hipError_t launch_gemv_t(const GemvArgs& a, int grid, hipStream_t stream) {
+    const size_t dyn = (size_t)a.K * sizeof(float);   // the x image
+    hipLaunchKernelGGL((gemv_kernel<NW, XL>), dim3(grid), dim3(NW * 64), dyn, stream, a);
+    return hipGetLastError();
+}
+
+// M == 1 dense stream: 1..4 waves of 32 KB slots beside the x image; x pieces
+// held in registers for the whole kernel when J == 16, else re-read every step.
+hipError_t launch_gemv(const GemvArgs& a, int grid, int nw, hipStream_t stream) {
+    const bool xl = a.J != 16;
+    switch (nw * 2 + (xl ? 1 : 0)) {
+        case 2: return launch_gemv_t<1, false>(a, grid, stream);
+        case 3: return launch_gemv_t<1, true>(a, grid, stream);
+        case 4: return launch_gemv_t<2, false>(a, grid, stream);
+        case 5: return launch_gemv_t<2, true>(a, grid, stream);
+        case 6: return launch_gemv_t<3, false>(a, grid, stream);
+        case 7: return launch_gemv_t<3, true>(a, grid, stream);
+        case 8: return launch_gemv_t<4, false>(a, grid, stream);
+        case 9: return launch_gemv_t<4, true>(a, grid, stream);
         default: return hipErrorInvalidValue;
     }
 }

@@ -43,30 +43,51 @@ def test_plan_numeric_fields_depend_on_k_only():
 
 
 def test_plan_is_pure_and_overrides_are_scheduling_only():
-    a = rg.rg_plan(1, 6144, 4096)
-    assert a == rg.rg_plan(1, 6144, 4096)
-    rg.rg_linear_set_launch(waves_per_wg=4, grid_wgs=100, depth=2, grid_order=1)
+    for shape, ov in (((4, 6144, 4096), (4, 100, 2)), ((1, 6144, 4096), (2, 100, 3))):
+        want = ov if shape[0] > 1 else (ov[0], ov[1], 0)
+        a = rg.rg_plan(*shape)
+        assert a == rg.rg_plan(*shape)
+        rg.rg_linear_set_launch(waves_per_wg=ov[0], grid_wgs=ov[1], depth=ov[2], grid_order=1)
+        try:
+            b = rg.rg_plan(*shape)
+            assert (b["waves_per_wg"], b["grid_wgs"], b["depth"]) == want
+            assert (b["order_id"], b["chunk"], b["nchunks"]) == (a["order_id"], a["chunk"], a["nchunks"])
+            assert b["kernel"] == a["kernel"]
+        finally:
+            rg.rg_linear_set_launch(None)
+        assert rg.rg_plan(*shape) == a
+
+
+def test_gemv_schedule_defaults():
+    # fewest rounds of quads per wave, then the fewest waves giving them, over all 256 workgroups
+    rg.rg_linear_set_launch(kernel="gemv")
     try:
-        b = rg.rg_plan(1, 6144, 4096)
-        assert (b["waves_per_wg"], b["grid_wgs"], b["depth"]) == (4, 100, 2)
-        assert (b["order_id"], b["chunk"], b["nchunks"]) == (a["order_id"], a["chunk"], a["nchunks"])
+        p = rg.rg_plan(1, 4096, 4096)
+        assert (p["kernel_name"], p["grid_wgs"], p["waves_per_wg"]) == ("gemv", 256, 4)
+        p = rg.rg_plan(1, 6144, 4096)            # 1536 quads: two rounds of 768 waves
+        assert (p["grid_wgs"], p["waves_per_wg"]) == (256, 3)
+        p = rg.rg_plan(1, 28672, 4096)           # 7168 quads: seven rounds of 1024 waves
+        assert (p["grid_wgs"], p["waves_per_wg"]) == (256, 4)
+        p = rg.rg_plan(1, 4096, 14336)           # x (56 KB) in LDS leaves room for 3 slots
+        assert p["waves_per_wg"] <= 3
     finally:
         rg.rg_linear_set_launch(None)
-    assert rg.rg_plan(1, 6144, 4096) == a
-
-
-def test_plan_kernel_choice():
-    assert rg.rg_plan(1, 6144, 4096)["kernel_name"] == "decode_xs"
-    assert rg.rg_plan(1, 8192, 28672)["kernel_name"] == "decode"     # J = 112 needs 7 waves
-    assert rg.rg_plan(4, 6144, 4096)["kernel_name"] == "decode"
-    assert rg.rg_plan(1, 10, 7)["kernel_name"] == "generic"     # K % 8 != 0
-    assert rg.rg_plan(16, 6144, 4096)["kernel_name"] == "decode"  # 4 slices of 4 rows
-    assert rg.rg_plan(65, 6144, 4096)["kernel_name"] == "tiled"
-    assert rg.rg_plan(2048, 57344, 8192)["kernel_name"] == "tiled"
+    rg.rg_linear_set_launch(kernel="gemv", waves_per_wg=4)
+    try:
+        with pytest.raises(rg.RgError):
+            rg.rg_plan(1, 4096, 14336)           # 4 slots + x do not fit
+        assert rg.rg_plan(1, 4096, 4096)["waves_per_wg"] == 4
+    finally:
+        rg.rg_linear_set_launch(None)
+    rg.rg_linear_set_launch(waves_per_wg=4)     # not forced: another kernel takes the shape
+    try:
+        assert rg.rg_plan(1, 4096, 14336)["kernel_name"] == "decode_xs"
+    finally:
+        rg.rg_linear_set_launch(None)
 
 
 def test_set_launch_range_checks():
-    for bad in (dict(waves_per_wg=9), dict(grid_wgs=-1), dict(depth=5), dict(grid_order=2), dict(kernel=7)):
+    for bad in (dict(waves_per_wg=9), dict(grid_wgs=-1), dict(depth=4), dict(depth=1), dict(grid_order=2), dict(kernel=6)):
         with pytest.raises(rg.RgError) as e:
             rg.rg_linear_set_launch(**bad)
         assert e.value.code == rg.RG_ERR_RANGE

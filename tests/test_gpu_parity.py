@@ -182,6 +182,56 @@ def test_ragged_shapes(M, N, K):
     _check_layer(M, N, K, seed=M * 1000 + K)
 
 
+@pytest.mark.parametrize("N", [1, 3, 4, 5, 1030, 2049])
+@pytest.mark.parametrize("K", [4096, 4352, 5120, 8192, 12288])
+def test_gemv_shapes(N, K):
+    """M = 1 dense stream: ragged quads (N % 4), steps with fewer than 16 segments (K / 256 % 16),
+    x in registers (K = 4096) or in LDS."""
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(kernel="gemv")
+    try:
+        assert rg.rg_plan(1, N, K)["kernel_name"] == "gemv"
+        _check_layer(1, N, K, seed=N + K)
+    finally:
+        rg.rg_linear_set_launch(None)
+
+
+@pytest.mark.parametrize("K,kernel", [(4352, "gemv"), (4096, "gemv"), (4096, "decode_xs")])
+def test_order_probes_inside_m1_rows(K, kernel):
+    """The hand-derived probes embedded in long rows (zero x and weight 1.0 around them) of an
+    otherwise random 1030-row layer, run by the M = 1 streaming kernels and compared bitwise
+    with the oracle on the same input."""
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(kernel=kernel)
+    try:
+        assert rg.rg_plan(1, 1030, K)["kernel_name"] == kernel
+        _probes_in_rows(K, 1030)
+    finally:
+        rg.rg_linear_set_launch(None)
+
+
+def _probes_in_rows(K, N):
+    import torch
+    import oracle
+    from tests import oracle_pins as pins
+    x0, w0 = gu.layer(1, N, K, seed=77)
+    X = np.zeros((1, K), dtype=np.float32)
+    W = np.array(w0, copy=True)
+    for i, p in enumerate(pins.load_probes()):
+        xp, wp = pins.probe_inputs(p)
+        X[:] = 0.0
+        X[0, :xp.shape[1]] = xp[0]
+        row = 3 + 97 * i
+        W[row] = 0x3F80
+        W[row, :wp.shape[1]] = wp[0]
+        xd, wd = gu.to_dev(X, W)
+        y = gu.run(xd, wd)
+        torch.cuda.synchronize()
+        want = oracle.linear_sampled(X, W, np.array([0]), np.array([row]))
+        got = gu.bits(y.cpu().numpy())[0, row]
+        assert int(got) == int(gu.bits(want)[0]), f"{p['name']} row {row}"
+
+
 @pytest.mark.parametrize("M,N,K", [(1, 10, 7), (2, 33, 301), (3, 5, 1), (1, 4, 257), (100, 1000, 1000)])
 def test_generic_shapes(M, N, K):
     _check_layer(M, N, K, seed=K)
@@ -237,10 +287,14 @@ def _launch_settings():
         dict(kernel="tiled", grid_order=1),
         dict(kernel="generic"),
         dict(kernel="generic", grid_wgs=3, grid_order=1),
+        dict(kernel="gemv"),
+        dict(kernel="gemv", waves_per_wg=1, grid_wgs=5, grid_order=1),
+        dict(kernel="gemv", waves_per_wg=2, grid_wgs=1000),
+        dict(kernel="gemv", waves_per_wg=3, grid_wgs=256, grid_order=1),
     ]
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 6144, 4096), (1, 4096, 14336), (3, 1000, 1000), (4, 2048, 2560),
+@pytest.mark.parametrize("M,N,K", [(1, 6144, 4096), (1, 1029, 4096), (1, 4096, 14336), (1, 1030, 4352), (3, 1000, 1000), (4, 2048, 2560),
                                    (16, 2048, 4096), (70, 1024, 1024)])
 def test_launch_settings_do_not_change_bits(M, N, K):
     import torch
