@@ -68,10 +68,12 @@ typedef enum {
 /* Kernel ids reported by rg_plan (scheduling only; the order is the same). */
 typedef enum {
     RG_KERNEL_GENERIC = 0,   /* one thread per output; any K, any alignment */
-    RG_KERNEL_DECODE = 1,    /* M <= 4: streaming GEMV / skinny GEMM, x in registers */
+    RG_KERNEL_DECODE = 1,    /* M <= 4 (or K < 4096 up to M = 64): streaming skinny GEMM, x in registers */
     RG_KERNEL_TILED = 2,     /* larger M: register-tiled kernel, whole K per workgroup */
     RG_KERNEL_DECODE_XS = 3, /* M == 1: streaming GEMV with x streamed through LDS beside W */
-    RG_KERNEL_GEMV = 4       /* M == 1, K % 256 == 0, K >= 4096: 32 KB W bursts, whole rows per wave */
+    RG_KERNEL_GEMV = 4,      /* M == 1, K % 256 == 0, K >= 4096: 32 KB W bursts, whole rows per wave */
+    RG_KERNEL_KTILE = 6      /* M <= 64: 4 x 4 register tiles, K segments shared out over thread groups
+                                (id 5 is not used) */
 } rg_kernel_id;
 
 /* Scheduling overrides for the determinism tests.  0 in a field = planner
@@ -81,10 +83,12 @@ typedef enum {
  *                   (a kernel that cannot handle the shape is not forced; the
  *                    call returns RG_ERR_RANGE)
  *   waves_per_wg  : 1..8  waves (64 threads each) per workgroup (gemv: 1..4, fewer
- *                   when x must fit in LDS beside the slots)
+ *                   when x must fit in LDS beside the slots; ktile: 4, or 8 with tile_n 16)
  *   grid_wgs      : 1..65536 workgroups (work is spread over them evenly)
  *   depth         : 2..3  decode pipeline depth in 128-byte-per-row slabs (unused by gemv)
  *   grid_order    : 0 = forward, 1 = reversed workgroup-to-rows mapping
+ *   tile_n        : 0 = planner default, else 16, 32 or 64: ktile's W rows per tile
+ *   reserved      : must be 0
  */
 typedef struct {
     int32_t kernel;
@@ -92,7 +96,8 @@ typedef struct {
     int32_t grid_wgs;
     int32_t depth;
     int32_t grid_order;
-    int32_t reserved[3];
+    int32_t tile_n;
+    int32_t reserved[2];
 } rg_launch_t;
 
 /* What rg_linear will do for a shape (on a 256-CU MI355X with default launch). */

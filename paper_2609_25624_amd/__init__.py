@@ -12,7 +12,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librg.so")
 
 RG_OK, RG_ERR_INVAL, RG_ERR_ALIGN, RG_ERR_ARCH, RG_ERR_HIP, RG_ERR_RANGE, RG_ERR_ALIAS = range(7)
-KERNELS = {0: "generic", 1: "decode", 2: "tiled", 3: "decode_xs", 4: "gemv"}
+KERNELS = {0: "generic", 1: "decode", 2: "tiled", 3: "decode_xs", 4: "gemv", 6: "ktile"}
 CHUNK = 256
 
 
@@ -27,7 +27,8 @@ class RgError(RuntimeError):
 
 class rg_launch_t(ctypes.Structure):
     _fields_ = [("kernel", ctypes.c_int32), ("waves_per_wg", ctypes.c_int32), ("grid_wgs", ctypes.c_int32),
-                ("depth", ctypes.c_int32), ("grid_order", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
+                ("depth", ctypes.c_int32), ("grid_order", ctypes.c_int32), ("tile_n", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 2)]
 
 
 class rg_plan_t(ctypes.Structure):
@@ -127,14 +128,14 @@ def rg_linear_ptr(x_ptr, w_ptr, y_ptr, M, N, K, stream_ptr=0):
 
 
 def rg_linear_set_launch(cfg=None, **kw):
-    """Scheduling overrides (kernel, waves_per_wg, grid_wgs, depth, grid_order); None resets."""
+    """Scheduling overrides (kernel, waves_per_wg, grid_wgs, depth, grid_order, tile_n); None resets."""
     if cfg is None and not kw:
         _check(lib.rg_linear_set_launch(None), "rg_linear_set_launch")
         return
     c = rg_launch_t()
     for k, v in dict(cfg or {}, **kw).items():
         if k == "kernel" and isinstance(v, str):
-            v = {"generic": 1, "decode": 2, "tiled": 3, "decode_xs": 4, "gemv": 5}[v]
+            v = {"generic": 1, "decode": 2, "tiled": 3, "decode_xs": 4, "gemv": 5, "ktile": 7}[v]
         setattr(c, k, int(v))
     _check(lib.rg_linear_set_launch(ctypes.byref(c)), "rg_linear_set_launch")
 

@@ -182,6 +182,37 @@ bool gemv_schedule(int64_t N, int64_t K, const rg_launch_t& o, Plan* p) {
     return true;
 }
 
+// Small-M tiles: BM rows of x (16, 32 or 64, the least that covers M up to
+// 64), BN columns of W, K shared out over 4096 / (BM * BN) thread groups.
+// Default BN (measured on the Llama-shaped layers): 16, or wider where N is
+// large enough to keep ~2 workgroups per CU with the wider tile (x is then
+// re-read from L2 fewer times).
+bool ktile_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan* p) {
+    const int bm = M <= 16 ? 16 : (M <= 32 ? 32 : 64);
+    int bn = o.tile_n;
+    if (bn == 0) {
+        bn = 16;
+        if (bm == 16 && ceil_div(N, 64) >= 448) bn = 64;
+        if (bm > 16 && ceil_div(N, 32) >= 896) bn = 32;
+    }
+    if (bn != 16 && bn != 32 && bn != 64) return false;
+    const int64_t tiles = ceil_div(M, bm) * ceil_div(N, bn);
+    if (tiles > 0x7fffffff) return false;
+    // 8 waves (twice the K groups) when the tiles alone would leave a CU with one wave
+    // per SIMD and K has a segment for every group
+    int nw = 4;
+    if (o.waves_per_wg > 0) nw = o.waves_per_wg;
+    else if (bn == 16 && tiles < 2 * kNominalCUs && ceil_div(K, rg::kChunk) >= 512 / bm) nw = 8;
+    if (nw != 4 && nw != 8) return false;
+    if (nw == 8 && bn != 16) return false;
+    p->tile_m = bm;
+    p->tile_n = bn;
+    p->grid = (int)tiles;
+    p->nw = nw;
+    p->depth = 0;
+    return true;
+}
+
 // The planner.  `fast_ok`: x and W 16-byte aligned and K % 8 == 0.
 int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& o, Plan* p) {
     const int64_t J = ceil_div(K, rg::kChunk);
@@ -195,7 +226,12 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     // M == 1: the 32 KB-burst kernel where one step covers K (J == 16); the
     // slab-streaming kernels elsewhere (they measure faster once x must be
     // re-read from LDS every step)
+    const bool ktile_ok = fast_ok && M <= kDecodeMaxM;
+    // ktile from M = 9 on; for 5 <= M <= 8 only where its 16 x 16 tiles are many (measured:
+    // the streaming decode kernel is faster on the narrow layers there)
+    const bool ktile_pref = M > 8 || (M > 4 && ceil_div(N, 16) >= 384);
     if (gemv_ok && ceil_div(K, rg::kChunk) == 16) want = RG_KERNEL_GEMV;
+    else if (ktile_ok && ktile_pref) want = RG_KERNEL_KTILE;
     else if (decode_ok && M <= kDecodeMaxM) want = (M == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;
     else if (tiled_ok) want = RG_KERNEL_TILED;
     const bool forced = o.kernel > 0;
@@ -205,10 +241,16 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         if (want == RG_KERNEL_DECODE_XS && M != 1) return RG_ERR_RANGE;
         if (want == RG_KERNEL_TILED && !tiled_ok) return RG_ERR_RANGE;
         if (want == RG_KERNEL_GEMV && !gemv_ok) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_KTILE && !ktile_ok) return RG_ERR_RANGE;
+        if (want == 5) return RG_ERR_RANGE;                      // unused kernel id
     }
     p->mslices = 1;
     p->kernel = want;
     p->reverse = o.grid_order;
+    if (want == RG_KERNEL_KTILE) {
+        if (ktile_schedule(M, N, K, o, p)) return RG_OK;
+        return RG_ERR_RANGE;
+    }
     if (want == RG_KERNEL_GEMV) {
         if (gemv_schedule(N, K, o, p)) return RG_OK;
         if (forced) return RG_ERR_RANGE;
@@ -256,7 +298,9 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
 }
 
 int validate_launch(const rg_launch_t& c) {
-    if (c.kernel < -1 || c.kernel > 5) return RG_ERR_RANGE;
+    if (c.kernel < -1 || c.kernel > 7) return RG_ERR_RANGE;
+    if (c.tile_n != 0 && c.tile_n != 16 && c.tile_n != 32 && c.tile_n != 64) return RG_ERR_RANGE;
+    if (c.reserved[0] != 0 || c.reserved[1] != 0) return RG_ERR_RANGE;
     if (c.waves_per_wg < 0 || c.waves_per_wg > 8) return RG_ERR_RANGE;
     if (c.grid_wgs < 0 || c.grid_wgs > 65536) return RG_ERR_RANGE;
     if (c.depth < 0 || c.depth > 3 || c.depth == 1) return RG_ERR_RANGE;
@@ -383,6 +427,8 @@ int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N,
         if (!p.x_streamed && blocks > 0x7fffffff) return RG_ERR_RANGE;
         e = p.x_streamed ? rg::launch_decode1(a, p.grid, p.nw, p.depth, st)
                          : rg::launch_decode(a, p.mt, (int)blocks, p.nw, p.depth, st);
+    } else if (p.kernel == RG_KERNEL_KTILE) {
+        e = rg::launch_ktile(x, w, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.reverse, st);
     } else if (p.kernel == RG_KERNEL_TILED) {
         e = rg::launch_tiled(x, w, y, M, N, K, p.tile_m, p.tile_n, p.reverse, st);
     } else {

@@ -44,6 +44,8 @@ hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipS
 hipError_t launch_gemv(const GemvArgs& a, int grid, int nw, hipStream_t stream);
 hipError_t launch_tiled(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
                         int reverse, hipStream_t stream);
+hipError_t launch_ktile(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
+                        int nt, int reverse, hipStream_t stream);
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream);
 hipError_t launch_argmax(const float* y, int64_t* out, int64_t M, int64_t N, hipStream_t stream);
 

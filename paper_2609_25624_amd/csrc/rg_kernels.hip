@@ -61,6 +61,26 @@ __device__ __forceinline__ void fmac8_bcast(float& acc, const float* x, const fl
           "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "v"(w[4]), "v"(w[5]), "v"(w[6]), "v"(w[7]), "n"(E));
 }
 
+// Four independent chains at once: for h = h0 .. h0+3, for m = 0..3:
+// acc[m] = fmaf(x_m[quad lane E][h], w[h], acc[m]).  Interleaving the four
+// accumulators keeps consecutive FMAs independent (each chain still sees its
+// own FMAs in ascending h), so the VALU does not stall on the previous result.
+template <int E>
+__device__ __forceinline__ void fmac4x4_bcast(float (&acc)[4], const float* x0, const float* x1, const float* x2,
+                                              const float* x3, const float* w) {
+#define RG_F(A, X, W) "v_fmac_f32_dpp %" #A ", %" #X ", %" #W " quad_perm:[%24,%24,%24,%24] row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+    asm("s_nop 1\n\t"
+        RG_F(0, 4, 20) RG_F(1, 8, 20) RG_F(2, 12, 20) RG_F(3, 16, 20)
+        RG_F(0, 5, 21) RG_F(1, 9, 21) RG_F(2, 13, 21) RG_F(3, 17, 21)
+        RG_F(0, 6, 22) RG_F(1, 10, 22) RG_F(2, 14, 22) RG_F(3, 18, 22)
+        RG_F(0, 7, 23) RG_F(1, 11, 23) RG_F(2, 15, 23) RG_F(3, 19, 23)
+        : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3])
+        : "v"(x0[0]), "v"(x0[1]), "v"(x0[2]), "v"(x0[3]), "v"(x1[0]), "v"(x1[1]), "v"(x1[2]), "v"(x1[3]),
+          "v"(x2[0]), "v"(x2[1]), "v"(x2[2]), "v"(x2[3]), "v"(x3[0]), "v"(x3[1]), "v"(x3[2]), "v"(x3[3]),
+          "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "n"(E));
+#undef RG_F
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) void*)p);
 }
@@ -180,14 +200,28 @@ __device__ __forceinline__ void fma_slab(const uint4 (&wp)[8], const float (&X)[
             float wv[8];
 #pragma unroll
             for (int h = 0; h < 8; ++h) wv[h] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+            if constexpr (MT == 4) {
+                // the four rows' chains interleaved, 4 elements at a time
 #pragma unroll
-            for (int m = 0; m < MT; ++m) {
-                const float* xb = &X[m][S][8 * (t & 1)];
-                switch (t >> 1) {
-                    case 0: fmac8_bcast<0>(acc[m], xb, wv); break;
-                    case 1: fmac8_bcast<1>(acc[m], xb, wv); break;
-                    case 2: fmac8_bcast<2>(acc[m], xb, wv); break;
-                    default: fmac8_bcast<3>(acc[m], xb, wv); break;
+                for (int hh = 0; hh < 8; hh += 4) {
+                    const int o = 8 * (t & 1) + hh;
+                    switch (t >> 1) {
+                        case 0: fmac4x4_bcast<0>(acc, &X[0][S][o], &X[1][S][o], &X[2][S][o], &X[3][S][o], &wv[hh]); break;
+                        case 1: fmac4x4_bcast<1>(acc, &X[0][S][o], &X[1][S][o], &X[2][S][o], &X[3][S][o], &wv[hh]); break;
+                        case 2: fmac4x4_bcast<2>(acc, &X[0][S][o], &X[1][S][o], &X[2][S][o], &X[3][S][o], &wv[hh]); break;
+                        default: fmac4x4_bcast<3>(acc, &X[0][S][o], &X[1][S][o], &X[2][S][o], &X[3][S][o], &wv[hh]); break;
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const float* xb = &X[m][S][8 * (t & 1)];
+                    switch (t >> 1) {
+                        case 0: fmac8_bcast<0>(acc[m], xb, wv); break;
+                        case 1: fmac8_bcast<1>(acc[m], xb, wv); break;
+                        case 2: fmac8_bcast<2>(acc[m], xb, wv); break;
+                        default: fmac8_bcast<3>(acc[m], xb, wv); break;
+                    }
                 }
             }
         }
@@ -807,6 +841,180 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
 }
 
 // ---------------------------------------------------------------------------
+// ktile kernel (small M, 4 < M <= 64): register tiles of 4 x 4 outputs with
+// the segments of K shared out over groups of threads.
+//
+// A workgroup of NT threads owns a BM x BN output tile and all of K.  Its
+// threads form KS groups of NT / KS; group g runs segments g, g + KS,
+// g + 2KS, ... (one segment per group per round), each thread a 4 x 4 tile
+// of chains over the segment in ascending k.  x (BM x KT floats) and up(W)
+// (BN x KT, widened once when staged) pass through LDS transposed, double
+// buffered, KT elements of every group's segment per barrier.  After a round
+// the groups' segment partials meet in LDS and group 0 folds them into its
+// running totals in ascending segment order (the first partial starts the
+// sum).  Splitting K this way gives small-M shapes enough independent work
+// for several waves per SIMD while the order stays the documented one.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int KS, int NT>
+__global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w,
+                                                   float* __restrict__ y, int64_t M, int64_t N, int64_t K,
+                                                   int reverse) {
+    static_assert(BM * BN * KS == 16 * NT, "NT threads x 16 outputs");
+    constexpr int TG = NT / KS;                      // threads per group
+    constexpr int KT = KS >= 8 ? 8 : 16;             // elements per slab
+    constexpr int NSL = kChunk / KT;                 // slabs per segment
+    constexpr int PADM = BM + 4, PADN = BN + 4;
+    constexpr int XPT = (BM * KT / 4 + TG - 1) / TG; // float4 x loads per thread
+    constexpr int WPT = (BN * KT / 8 + TG - 1) / TG; // uint4 W loads per thread
+    __shared__ __attribute__((aligned(16))) float xs[KS][2][KT][PADM];
+    __shared__ __attribute__((aligned(16))) float ws[KS][2][KT][PADN];
+    __shared__ __attribute__((aligned(16))) float part[KS > 1 ? KS - 1 : 1][TG][16];
+
+    const int tid = threadIdx.x;
+    const int g = tid / TG, tg = tid % TG;
+    const int mi = tg % (BM / 4), ni = tg / (BM / 4);
+    const int64_t tiles_n = (N + BN - 1) / BN;
+    const int64_t b = reverse ? (int64_t)(gridDim.x - 1 - blockIdx.x) : (int64_t)blockIdx.x;
+    const int64_t m0 = (b / tiles_n) * BM, n0 = (b % tiles_n) * BN;
+    const int J = (int)((K + kChunk - 1) / kChunk);
+    const int rounds = (J + KS - 1) / KS;
+
+    float4 xr[XPT];
+    uint4 wr[WPT];
+    // slab sl of this group's segment in round t
+    auto load_slab = [&](int t, int sl) {
+        const int64_t j = (int64_t)t * KS + g;
+        const int64_t k0 = j * kChunk + (int64_t)sl * KT;
+#pragma unroll
+        for (int u = 0; u < XPT; ++u) {
+            const int idx = tg + TG * u;                  // over BM rows x KT/4 float4
+            const int row = idx / (KT / 4), kq = idx % (KT / 4);
+            const int64_t gm = m0 + row, gk = k0 + 4 * kq;
+            const bool ok = idx < BM * KT / 4 && j < J && gm < M && gk + 4 <= K;
+            xr[u] = ok ? *reinterpret_cast<const float4*>(x + gm * K + gk) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < WPT; ++u) {
+            const int idx = tg + TG * u;                  // over BN rows x KT/8 uint4
+            const int row = idx / (KT / 8), kh = idx % (KT / 8);
+            const int64_t gn = n0 + row, gk = k0 + 8 * kh;
+            const bool ok = idx < BN * KT / 8 && j < J && gn < N && gk + 8 <= K;
+            wr[u] = ok ? *reinterpret_cast<const uint4*>(w + gn * K + gk) : make_uint4(0u, 0u, 0u, 0u);
+        }
+    };
+    auto store_slab = [&](int buf) {
+#pragma unroll
+        for (int u = 0; u < XPT; ++u) {
+            const int idx = tg + TG * u;
+            if (idx < BM * KT / 4) {
+                const int row = idx / (KT / 4), kq = idx % (KT / 4);
+                xs[g][buf][4 * kq + 0][row] = xr[u].x;
+                xs[g][buf][4 * kq + 1][row] = xr[u].y;
+                xs[g][buf][4 * kq + 2][row] = xr[u].z;
+                xs[g][buf][4 * kq + 3][row] = xr[u].w;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < WPT; ++u) {
+            const int idx = tg + TG * u;
+            if (idx < BN * KT / 8) {
+                const int row = idx / (KT / 8), kh = idx % (KT / 8);
+                const uint32_t d[4] = {wr[u].x, wr[u].y, wr[u].z, wr[u].w};
+#pragma unroll
+                for (int h = 0; h < 8; ++h) ws[g][buf][8 * kh + h][row] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+            }
+        }
+    };
+
+    float acc[16], tot[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tot[i] = 0.0f;
+
+    load_slab(0, 0);
+    store_slab(0);
+    __syncthreads();
+    int buf = 0;
+    for (int t = 0; t < rounds; ++t) {
+        const int64_t j = (int64_t)t * KS + g;
+        const int len = j < J ? (int)min((int64_t)kChunk, K - j * kChunk) : 0;   // this group's segment length
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+        for (int sl = 0; sl < NSL; ++sl) {
+            const bool more = sl + 1 < NSL || t + 1 < rounds;
+            if (more) load_slab(sl + 1 < NSL ? t : t + 1, sl + 1 < NSL ? sl + 1 : 0);
+            const int kvalid = max(0, min(KT, len - sl * KT));
+            if (kvalid == KT) {
+#pragma unroll
+                for (int kk = 0; kk < KT; ++kk) {
+                    const float4 xv = *reinterpret_cast<const float4*>(&xs[g][buf][kk][4 * mi]);
+                    const float4 wv = *reinterpret_cast<const float4*>(&ws[g][buf][kk][4 * ni]);
+                    const float xa[4] = {xv.x, xv.y, xv.z, xv.w}, wa[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) acc[4 * r + c] = __builtin_fmaf(xa[r], wa[c], acc[4 * r + c]);
+                }
+            } else {
+                for (int kk = 0; kk < kvalid; ++kk) {
+                    const float4 xv = *reinterpret_cast<const float4*>(&xs[g][buf][kk][4 * mi]);
+                    const float4 wv = *reinterpret_cast<const float4*>(&ws[g][buf][kk][4 * ni]);
+                    const float xa[4] = {xv.x, xv.y, xv.z, xv.w}, wa[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) acc[4 * r + c] = __builtin_fmaf(xa[r], wa[c], acc[4 * r + c]);
+                }
+            }
+            if (more) {
+                store_slab(buf ^ 1);
+                __syncthreads();
+                buf ^= 1;
+            }
+        }
+        // the round's segment partials, folded by group 0 in ascending segment order
+        if constexpr (KS > 1) {
+            if (g > 0) {
+#pragma unroll
+                for (int i = 0; i < 16; i += 4)
+                    *reinterpret_cast<float4*>(&part[g - 1][tg][i]) = make_float4(acc[i], acc[i + 1], acc[i + 2], acc[i + 3]);
+            }
+            __syncthreads();
+        }
+        if (g == 0) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) tot[i] = (t == 0) ? acc[i] : tot[i] + acc[i];
+            if constexpr (KS > 1) {
+                for (int gg = 1; gg < KS; ++gg) {
+                    if ((int64_t)t * KS + gg >= J) break;
+#pragma unroll
+                    for (int i = 0; i < 16; i += 4) {
+                        const float4 pv = *reinterpret_cast<const float4*>(&part[gg - 1][tg][i]);
+                        tot[i] = tot[i] + pv.x;
+                        tot[i + 1] = tot[i + 1] + pv.y;
+                        tot[i + 2] = tot[i + 2] + pv.z;
+                        tot[i + 3] = tot[i + 3] + pv.w;
+                    }
+                }
+            }
+        }
+        // part[] is written again only after the next round's slab barriers, which group 0
+        // reaches after this fold
+    }
+    if (g == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t gm = m0 + 4 * mi + r;
+            if (gm >= M) continue;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int64_t gn = n0 + 4 * ni + c;
+                if (gn < N) y[gm * N + gn] = tot[4 * r + c];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // gemv kernel (M == 1, K a multiple of 256 with at least 16 segments):
 // dense weight stream.
 //
@@ -1180,6 +1388,25 @@ hipError_t launch_tiled(const float* x, const uint16_t* w, float* y, int64_t M, 
     else if (bm == 64 && bn == 64) hipLaunchKernelGGL((tiled_kernel<64, 64>), grid, block, 0, stream, x, w, y, M, N, K, reverse);
     else return hipErrorInvalidValue;
     return hipGetLastError();
+}
+
+// Small-M tiles (16 outputs per thread, K shared out over KS = 16 * nt / (bm * bn) groups).
+hipError_t launch_ktile(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
+                        int nt, int reverse, hipStream_t stream) {
+    const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+    if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)tiles);
+#define RG_KT(BM, BN, NT) \
+    if (bm == BM && bn == BN && nt == NT) { \
+        hipLaunchKernelGGL((ktile_kernel<BM, BN, 16 * NT / (BM * BN), NT>), grid, dim3(NT), 0, stream, x, w, y, M, N, K, \
+                           reverse); \
+        return hipGetLastError(); \
+    }
+    RG_KT(16, 16, 256) RG_KT(16, 32, 256) RG_KT(16, 64, 256) RG_KT(32, 16, 256) RG_KT(32, 32, 256) RG_KT(32, 64, 256)
+    RG_KT(64, 16, 256) RG_KT(64, 32, 256) RG_KT(64, 64, 256)
+    RG_KT(16, 16, 512) RG_KT(32, 16, 512) RG_KT(64, 16, 512)
+#undef RG_KT
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream) {

@@ -196,6 +196,22 @@ def test_gemv_shapes(N, K):
         rg.rg_linear_set_launch(None)
 
 
+@pytest.mark.parametrize("M", [2, 5, 9, 16, 17, 33, 64])
+@pytest.mark.parametrize("N,K", [(3, 4096), (1030, 4104), (301, 8192), (130, 14336), (77, 520)])
+@pytest.mark.parametrize("tile_n,waves", [(0, 0), (16, 4), (16, 8), (32, 0), (64, 0)])
+def test_ktile_shapes(M, N, K, tile_n, waves):
+    """Small-M tiles with K shared out over thread groups: partial tiles in M and N, a short
+    last segment (K % 256 != 0), rounds where only some groups have a segment (J % KS != 0),
+    every tile width."""
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(kernel="ktile", tile_n=tile_n, waves_per_wg=waves)
+    try:
+        assert rg.rg_plan(M, N, K)["kernel_name"] == "ktile"
+        _check_layer(M, N, K, seed=M * 7 + N + K)
+    finally:
+        rg.rg_linear_set_launch(None)
+
+
 @pytest.mark.parametrize("K,kernel", [(4352, "gemv"), (4096, "gemv"), (4096, "decode_xs")])
 def test_order_probes_inside_m1_rows(K, kernel):
     """The hand-derived probes embedded in long rows (zero x and weight 1.0 around them) of an
@@ -291,11 +307,16 @@ def _launch_settings():
         dict(kernel="gemv", waves_per_wg=1, grid_wgs=5, grid_order=1),
         dict(kernel="gemv", waves_per_wg=2, grid_wgs=1000),
         dict(kernel="gemv", waves_per_wg=3, grid_wgs=256, grid_order=1),
+        dict(kernel="ktile"),
+        dict(kernel="ktile", tile_n=16, grid_order=1),
+        dict(kernel="ktile", tile_n=32),
+        dict(kernel="ktile", tile_n=64, grid_order=1),
+        dict(kernel="ktile", tile_n=16, waves_per_wg=8),
     ]
 
 
 @pytest.mark.parametrize("M,N,K", [(1, 6144, 4096), (1, 1029, 4096), (1, 4096, 14336), (1, 1030, 4352), (3, 1000, 1000), (4, 2048, 2560),
-                                   (16, 2048, 4096), (70, 1024, 1024)])
+                                   (16, 2048, 4096), (37, 1030, 4352), (70, 1024, 1024)])
 def test_launch_settings_do_not_change_bits(M, N, K):
     import torch
     import paper_2609_25624_amd as rg
