@@ -72,8 +72,8 @@ typedef enum {
     RG_KERNEL_TILED = 2,     /* larger M: register-tiled kernel, whole K per workgroup */
     RG_KERNEL_DECODE_XS = 3, /* M == 1: streaming GEMV with x streamed through LDS beside W */
     RG_KERNEL_GEMV = 4,      /* M == 1, K % 256 == 0, K >= 4096: 32 KB W bursts, whole rows per wave */
-    RG_KERNEL_KTILE = 6      /* M <= 64: 4 x 4 register tiles, K segments shared out over thread groups
-                                (id 5 is not used) */
+    RG_KERNEL_KTILE = 6      /* 4 < M <= 64 (any M when forced): 4 x 4 register tiles, K segments
+                                shared out over thread groups (id 5 is not used) */
 } rg_kernel_id;
 
 /* Scheduling overrides for the determinism tests.  0 in a field = planner

@@ -188,7 +188,7 @@ bool gemv_schedule(int64_t N, int64_t K, const rg_launch_t& o, Plan* p) {
 // large enough to keep ~2 workgroups per CU with the wider tile (x is then
 // re-read from L2 fewer times).
 bool ktile_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan* p) {
-    const int bm = M <= 16 ? 16 : (M <= 32 ? 32 : 64);
+    const int bm = M <= 16 ? 16 : (M <= 32 ? 32 : 64);   // M > 64 (forced): 64-row tiles
     int bn = o.tile_n;
     if (bn == 0) {
         bn = 16;
@@ -241,7 +241,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         if (want == RG_KERNEL_DECODE_XS && M != 1) return RG_ERR_RANGE;
         if (want == RG_KERNEL_TILED && !tiled_ok) return RG_ERR_RANGE;
         if (want == RG_KERNEL_GEMV && !gemv_ok) return RG_ERR_RANGE;
-        if (want == RG_KERNEL_KTILE && !ktile_ok) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_KTILE && !fast_ok) return RG_ERR_RANGE;   // any M when forced
         if (want == 5) return RG_ERR_RANGE;                      // unused kernel id
     }
     p->mslices = 1;

@@ -196,13 +196,13 @@ def test_gemv_shapes(N, K):
         rg.rg_linear_set_launch(None)
 
 
-@pytest.mark.parametrize("M", [2, 5, 9, 16, 17, 33, 64])
+@pytest.mark.parametrize("M", [2, 5, 9, 16, 17, 33, 64, 100])
 @pytest.mark.parametrize("N,K", [(3, 4096), (1030, 4104), (301, 8192), (130, 14336), (77, 520)])
 @pytest.mark.parametrize("tile_n,waves", [(0, 0), (16, 4), (16, 8), (32, 0), (64, 0)])
 def test_ktile_shapes(M, N, K, tile_n, waves):
     """Small-M tiles with K shared out over thread groups: partial tiles in M and N, a short
     last segment (K % 256 != 0), rounds where only some groups have a segment (J % KS != 0),
-    every tile width."""
+    every tile width, and (forced) more than one tile of rows."""
     import paper_2609_25624_amd as rg
     rg.rg_linear_set_launch(kernel="ktile", tile_n=tile_n, waves_per_wg=waves)
     try:
