@@ -167,18 +167,21 @@ def trace_summary(path, args):
     """Per-layer kernel durations from a rocprofv3 kernel trace of this script.
 
     The library's dispatches come in a fixed order: warmup and timed steps
-    (four layers each), then per layer 10 untimed and --per-layer-calls timed
-    calls, then one call per layer for the exactness check.  The durations of
-    each layer's timed block are the ones the per-layer event timing reports."""
+    (four layers each), then per layer 10 untimed calls, 5 timed loops of
+    --per-layer-calls, 3 untimed and --per-layer-calls warm calls, then one
+    call per layer for the exactness check.  The durations of each layer's 5
+    timed loops are the ones the per-layer event timing reports (as a median
+    of loop means; here their overall mean)."""
     rows = [r for r in _csv_rows(path) if "rg::" in r["Kernel_Name"] and "cast_kernel" not in r["Kernel_Name"]
             and "argmax_kernel" not in r["Kernel_Name"]]
     dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
     i = (args.warmup + args.steps) * len(LAYERS)
     lines = [f"dispatches of the library's linear kernels: {len(rows)}",
              f"{'layer':8s} {'kernel':40s} {'calls':>5s} {'avg_us':>8s} {'min_us':>8s} {'max_us':>8s} {'TB/s':>6s}"]
+    R = args.per_layer_calls
     for name, N, K in LAYERS:
-        blk = rows[i + 10:i + 10 + args.per_layer_calls]
-        i += 10 + args.per_layer_calls
+        blk = rows[i + 10:i + 10 + 5 * R]
+        i += 10 + 5 * R + 3 + R
         d = [dur(r) for r in blk]
         avg = sum(d) / len(d)
         lines.append(f"{name:8s} {blk[0]['Kernel_Name'][:40]:40s} {len(d):5d} {avg:8.3f} {min(d):8.3f} {max(d):8.3f} "
@@ -301,24 +304,40 @@ def main():
     ms_per_step = t0.elapsed_time(t1) / args.steps
     value_tbs = step_wbytes / (ms_per_step * 1e-3) / 1e12
 
-    # ---- per-layer us/call (same rotation, same stream) ----
+    # ---- per-layer us/call: median of 5 loops of R calls (same rotation, same stream),
+    # then the warm figure (one weight copy, reused from the caches) ----
     per_layer = {}
     for L in layers:
         R = args.per_layer_calls
         for i in range(10):
             rg.rg_linear(L["xd"], L["ws"][i % len(L["ws"])], L["y"], stream=stream)
+        loops = []
+        for rep in range(5):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for i in range(R):
+                rg.rg_linear(L["xd"], L["ws"][i % len(L["ws"])], L["y"], stream=stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            loops.append(a.elapsed_time(b) * 1e3 / R)
+        us = sorted(loops)[2]
+        for i in range(3):
+            rg.rg_linear(L["xd"], L["ws"][0], L["y"], stream=stream)
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
         a.record(stream)
         for i in range(R):
-            rg.rg_linear(L["xd"], L["ws"][i % len(L["ws"])], L["y"], stream=stream)
+            rg.rg_linear(L["xd"], L["ws"][0], L["y"], stream=stream)
         b.record(stream)
         torch.cuda.synchronize()
-        us = a.elapsed_time(b) * 1e3 / R
+        warm_us = a.elapsed_time(b) * 1e3 / R
         per_layer[L["name"]] = dict(
             N=L["N"], K=L["K"], us_per_call=round(us, 3),
+            us_per_call_loops=[round(v, 3) for v in loops], us_mean=round(sum(loops) / len(loops), 3),
             weight_TBs=round(L["wbytes"] / (us * 1e-6) / 1e12, 4),
             frac_of_8TBs=round(L["wbytes"] / (us * 1e-6) / (HBM_PEAK_GBS * 1e9), 4),
+            warm_us_per_call=round(warm_us, 3),
             kernel=L["plan"]["kernel_name"], waves_per_wg=L["plan"]["waves_per_wg"],
             grid_wgs=L["plan"]["grid_wgs"], rotated_copies=len(L["ws"]))
 
@@ -354,21 +373,30 @@ def main():
                 rg.rg_cast_bf16_f32(L["ws"][i % len(L["ws"])], wt, stream=stream)
                 torch.matmul(L["xd"], wt.t(), out=L["y"])
 
-        R = max(20, args.steps // 3)
-        for i in range(5):
-            scheme_step(i)
-        torch.cuda.synchronize()
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for i in range(R):
-            scheme_step(i)
-        b.record(stream)
-        torch.cuda.synchronize()
-        sms = a.elapsed_time(b) / R
-        scheme = dict(ms_per_step=round(sms, 4), speedup_of_fused=round(sms / ms_per_step, 3),
+        def gemm_step(i):
+            for L in layers:
+                torch.matmul(L["xd"], tmp[L["name"]].t(), out=L["y"])
+
+        def timed(fn):
+            R = max(20, args.steps // 3)
+            for i in range(5):
+                fn(i)
+            torch.cuda.synchronize()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for i in range(R):
+                fn(i)
+            b.record(stream)
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / R
+
+        sms = timed(scheme_step)
+        gms = timed(gemm_step)
+        scheme = dict(ms_per_step=round(sms, 4), gemm_only_ms_per_step=round(gms, 4),
+                      speedup_of_fused=round(sms / ms_per_step, 3),
                       transient_fp32_bytes=int(max(4 * L["N"] * L["K"] for L in layers)),
-                      gemm="torch.matmul float32 (vendor BLAS)")
+                      gemm="torch.matmul float32 (vendor BLAS); the GEMM-only figure reuses one FP32 copy")
         del tmp
 
     # ---- CPU oracle on the host: bounded sample of the same step ----

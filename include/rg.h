@@ -1,7 +1,7 @@
 /*
  * rg.h -- C-ABI of a bit-reproducible fused-upcast linear layer for AMD MI355X (gfx950).
  *
- * The operation (paper: Design, eq. 2, with the bias term left out):
+ * The operation (paper: Design, eq. 2; rg_linear_bias adds its bias term):
  *
  *     y[m][n] = sum over k of  x[m][k] * up(W[n][k])
  *
@@ -127,6 +127,18 @@ typedef struct {
  */
 int rg_linear(const float* x, const uint16_t* w_bf16, float* y, int64_t M, int64_t N, int64_t K,
               void* stream);
+
+/*
+ * y = x * up(W)^T + b: the product of rg_linear in RG-ORDER-1, then one
+ * binary32 round-to-nearest-even addition of b[n] per output (Design, eq. 2
+ * with its bias term; the bias is added after the fold, never into a chain).
+ *   bias   device pointer, float32 [N], 4-byte aligned, not NULL, must not
+ *          overlap y (it may alias x or W, which are only read)
+ * Everything else as rg_linear (same kernels, same scheduling, same errors;
+ * RG_ERR_INVAL for a NULL bias).
+ */
+int rg_linear_bias(const float* x, const uint16_t* w_bf16, const float* bias, float* y, int64_t M, int64_t N,
+                   int64_t K, void* stream);
 
 /* Set (cfg != NULL) or reset (cfg == NULL) the scheduling overrides used by
  * later rg_linear calls.  RG_ERR_RANGE if a field is out of range. */

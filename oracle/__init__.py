@@ -28,6 +28,8 @@ def lib():
         L.rg_oracle_dot.restype = ctypes.c_float
         L.rg_oracle_linear.argtypes = [vp, vp, vp, i64, i64, i64, ci]
         L.rg_oracle_linear.restype = ci
+        L.rg_oracle_linear_bias.argtypes = [vp, vp, vp, vp, i64, i64, i64, ci]
+        L.rg_oracle_linear_bias.restype = ci
         L.rg_oracle_linear_sampled.argtypes = [vp, vp, i64, vp, vp, i64, vp, ci]
         L.rg_oracle_linear_sampled.restype = ci
         L.rg_ref_fp64.argtypes = [vp, vp, vp, vp, i64, i64, i64, ci]
@@ -63,6 +65,22 @@ def linear(x, w, nthreads=None) -> np.ndarray:
     rc = lib().rg_oracle_linear(x.ctypes.data, w.ctypes.data, y.ctypes.data, M, N, K, _threads(nthreads))
     if rc != 0:
         raise ValueError("rg_oracle_linear rejected its arguments")
+    return y
+
+
+def linear_bias(x, w, b, nthreads=None) -> np.ndarray:
+    """y[M,N] = (the documented order) + b[N], one binary32 addition after the fold."""
+    x, w = _check(x, w)
+    b = np.ascontiguousarray(b, dtype=np.float32)
+    M, K = x.shape
+    N = w.shape[0]
+    if b.shape != (N,):
+        raise ValueError(f"bias shape {b.shape}, expected ({N},)")
+    y = np.empty((M, N), dtype=np.float32)
+    rc = lib().rg_oracle_linear_bias(x.ctypes.data, w.ctypes.data, b.ctypes.data, y.ctypes.data, M, N, K,
+                                     _threads(nthreads))
+    if rc != 0:
+        raise ValueError("rg_oracle_linear_bias rejected its arguments")
     return y
 
 

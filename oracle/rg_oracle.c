@@ -19,6 +19,10 @@
  *   y      = p_0, then for j = 1 .. J-1 ascending:  y = y + p_j
  *            (partials combined in fixed ascending segment order, rule R3)
  *
+ * With a bias (rg_oracle_linear_bias): y[m,n] = (the fold above) + b[n], one
+ * binary32 addition after the last segment (Design, eq. 2's "+ b"; the bias
+ * never enters a segment chain).
+ *
  * Nothing depends on m, n or M (batch invariance by construction, rule R4).
  * Arithmetic is IEEE-754 binary32, round to nearest even, gradual underflow:
  * this file is compiled with -ffp-contract=off and without fast-math, and
@@ -69,6 +73,20 @@ int rg_oracle_linear(const float* x, const uint16_t* w, float* y, int64_t M, int
     for (int64_t i = 0; i < total; ++i) {
         const int64_t m = i / N, n = i % N;
         y[i] = rg_oracle_dot(x + m * K, w + n * K, K);
+    }
+    return 0;
+}
+
+/* y[m][n] = rg_oracle_dot(x_m, w_n) + b[n]: the fold, then one addition. */
+int rg_oracle_linear_bias(const float* x, const uint16_t* w, const float* b, float* y, int64_t M, int64_t N,
+                          int64_t K, int nthreads) {
+    if (M < 0 || N < 0 || K < 1 || !b) return -1;
+    const int64_t total = M * N;
+#pragma omp parallel for schedule(dynamic, 64) num_threads(nthreads > 0 ? nthreads : 1)
+    for (int64_t i = 0; i < total; ++i) {
+        const int64_t m = i / N, n = i % N;
+        const float d = rg_oracle_dot(x + m * K, w + n * K, K);
+        y[i] = d + b[n];
     }
     return 0;
 }

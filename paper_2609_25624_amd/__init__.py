@@ -51,6 +51,7 @@ def _load():
     vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
     sig = {
         "rg_linear": [vp, vp, vp, i64, i64, i64, vp],
+        "rg_linear_bias": [vp, vp, vp, vp, i64, i64, i64, vp],
         "rg_linear_set_launch": [ctypes.POINTER(rg_launch_t)],
         "rg_plan": [i64, i64, i64, ctypes.POINTER(rg_plan_t)],
         "rg_cast_bf16_f32": [vp, vp, i64, vp],
@@ -72,7 +73,7 @@ def _load():
 lib = _load()
 
 # Every symbol include/rg.h declares (checked by the tests).
-EXPORTS = ("rg_linear", "rg_linear_set_launch", "rg_plan", "rg_cast_bf16_f32", "rg_argmax_rows",
+EXPORTS = ("rg_linear", "rg_linear_bias", "rg_linear_set_launch", "rg_plan", "rg_cast_bf16_f32", "rg_argmax_rows",
            "rg_stream_create_cu_mask", "rg_stream_destroy", "rg_device_cu_count", "rg_strerror",
            "rg_last_hip_error")
 
@@ -119,6 +120,23 @@ def rg_linear(x, w, y, stream=None):
     if w.shape[1] != K or tuple(y.shape) != (M, N):
         raise ValueError(f"shape mismatch x{tuple(x.shape)} w{tuple(w.shape)} y{tuple(y.shape)}")
     _check(lib.rg_linear(px, pw, py, M, N, K, _stream_ptr(stream)), "rg_linear")
+    return y
+
+
+def rg_linear_bias(x, w, b, y, stream=None):
+    """y[M,N] = x[M,K] * up(w[N,K])^T + b[N]: the fixed-order product, then one add of b."""
+    import torch
+    px = _tensor_ptr(x, (torch.float32,), "x")
+    pw = _tensor_ptr(w, (torch.bfloat16, torch.int16, torch.uint16), "w")
+    pb = _tensor_ptr(b, (torch.float32,), "b")
+    py = _tensor_ptr(y, (torch.float32,), "y")
+    if x.dim() != 2 or w.dim() != 2 or y.dim() != 2 or b.dim() != 1:
+        raise ValueError("x, w, y must be 2-D and b 1-D")
+    M, K = x.shape
+    N = w.shape[0]
+    if w.shape[1] != K or tuple(y.shape) != (M, N) or b.shape[0] != N:
+        raise ValueError(f"shape mismatch x{tuple(x.shape)} w{tuple(w.shape)} b{tuple(b.shape)} y{tuple(y.shape)}")
+    _check(lib.rg_linear_bias(px, pw, pb, py, M, N, K, _stream_ptr(stream)), "rg_linear_bias")
     return y
 
 

@@ -373,12 +373,19 @@ int rg_plan(int64_t M, int64_t N, int64_t K, rg_plan_t* out) {
     return RG_OK;
 }
 
-int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The one implementation behind rg_linear and rg_linear_bias (bias may be null).
+int linear_impl(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                void* stream) {
     if (!x || !w || !y || M < 1 || N < 1 || K < 1) return RG_ERR_INVAL;
     if (!mul_ok(M, K) || !mul_ok(N, K) || !mul_ok(M, N)) return RG_ERR_INVAL;
-    if (((uintptr_t)x & 3) || ((uintptr_t)w & 1) || ((uintptr_t)y & 3)) return RG_ERR_ALIGN;
+    if (((uintptr_t)x & 3) || ((uintptr_t)w & 1) || ((uintptr_t)y & 3) || ((uintptr_t)bias & 3)) return RG_ERR_ALIGN;
     if (overlaps(y, (size_t)(M * N) * 4, x, (size_t)(M * K) * 4) ||
-        overlaps(y, (size_t)(M * N) * 4, w, (size_t)(N * K) * 2))
+        overlaps(y, (size_t)(M * N) * 4, w, (size_t)(N * K) * 2) ||
+        (bias && overlaps(y, (size_t)(M * N) * 4, bias, (size_t)N * 4)))
         return RG_ERR_ALIAS;
     int cus = 0;
     const int dc = device_check(&cus);
@@ -394,6 +401,7 @@ int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N,
         rg::GemvArgs a;
         a.x = x;
         a.w = w;
+        a.bias = bias;
         a.y = y;
         a.N = N;
         a.K = K;
@@ -408,6 +416,7 @@ int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N,
         rg::DecodeArgs a;
         a.x = x;
         a.w = w;
+        a.bias = bias;
         a.y = y;
         a.M = M;
         a.N = N;
@@ -428,13 +437,27 @@ int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N,
         e = p.x_streamed ? rg::launch_decode1(a, p.grid, p.nw, p.depth, st)
                          : rg::launch_decode(a, p.mt, (int)blocks, p.nw, p.depth, st);
     } else if (p.kernel == RG_KERNEL_KTILE) {
-        e = rg::launch_ktile(x, w, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.reverse, st);
+        e = rg::launch_ktile(x, w, bias, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.reverse, st);
     } else if (p.kernel == RG_KERNEL_TILED) {
-        e = rg::launch_tiled(x, w, y, M, N, K, p.tile_m, p.tile_n, p.reverse, st);
+        e = rg::launch_tiled(x, w, bias, y, M, N, K, p.tile_m, p.tile_n, p.reverse, st);
     } else {
-        e = rg::launch_generic(x, w, y, M, N, K, p.grid, p.reverse, st);
+        e = rg::launch_generic(x, w, bias, y, M, N, K, p.grid, p.reverse, st);
     }
     return hip_status(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, void* stream) {
+    return linear_impl(x, w, nullptr, y, M, N, K, stream);
+}
+
+int rg_linear_bias(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                   void* stream) {
+    if (!bias) return RG_ERR_INVAL;
+    return linear_impl(x, w, bias, y, M, N, K, stream);
 }
 
 int rg_cast_bf16_f32(const uint16_t* w, float* o, int64_t count, void* stream) {

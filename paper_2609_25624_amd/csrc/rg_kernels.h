@@ -10,6 +10,7 @@ constexpr int kChunk = 256;  // segment length C of the documented order
 struct DecodeArgs {
     const float* x;
     const uint16_t* w;
+    const float* bias;  // b[N] added after the fold, or null
     float* y;
     int64_t M, N, K;
     int64_t Q;          // quads of W rows: ceil(N / 4)
@@ -28,6 +29,7 @@ struct DecodeArgs {
 struct GemvArgs {
     const float* x;
     const uint16_t* w;
+    const float* bias;  // b[N] added after the fold, or null
     float* y;
     int64_t N, K;
     int64_t qbase;      // Q / V quads per wave (Q = ceil(N / 4), V = waves in the grid) ...
@@ -37,15 +39,15 @@ struct GemvArgs {
     int reverse;        // 1: workgroup b takes the quads of workgroup grid-1-b
 };
 
-hipError_t launch_generic(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K,
-                          int grid, int reverse, hipStream_t stream);
+hipError_t launch_generic(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N,
+                          int64_t K, int grid, int reverse, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_gemv(const GemvArgs& a, int grid, int nw, hipStream_t stream);
-hipError_t launch_tiled(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
-                        int reverse, hipStream_t stream);
-hipError_t launch_ktile(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
-                        int nt, int reverse, hipStream_t stream);
+hipError_t launch_tiled(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int reverse, hipStream_t stream);
+hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int nt, int reverse, hipStream_t stream);
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream);
 hipError_t launch_argmax(const float* y, int64_t* out, int64_t M, int64_t N, hipStream_t stream);
 

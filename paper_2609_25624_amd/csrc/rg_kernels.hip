@@ -1,6 +1,6 @@
 // Fused-upcast linear layer kernels for gfx950 (MI355X).
 //
-// Every kernel here computes y[m][n] = sum_k x[m][k] * up(W[n][k]) in the one
+// Every kernel here computes y[m][n] = sum_k x[m][k] * up(W[n][k]) (+ b[n]) in the one
 // order documented in include/rg.h ("RG-ORDER-1"): 256-wide K segments, each a
 // chain of fmaf from +0 in ascending k, segment partials folded left to right
 // in ascending segment order (paper: Design, eq. 2 and rules R1-R4).  Kernels
@@ -140,7 +140,7 @@ __device__ __forceinline__ float fold_partials(const float* p, int J) {
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) generic_kernel(const float* __restrict__ x,
                                                       const uint16_t* __restrict__ w,
-                                                      float* __restrict__ y, int64_t M, int64_t N,
+                                                      const float* __restrict__ bias, float* __restrict__ y, int64_t M, int64_t N,
                                                       int64_t K, int reverse) {
     const int64_t total = M * N;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -156,7 +156,7 @@ __global__ void __launch_bounds__(256) generic_kernel(const float* __restrict__ 
             for (int64_t k = k0; k < k1; ++k) p = __builtin_fmaf(xr[k], up1(wr[k]), p);
             acc = (j == 0) ? p : acc + p;
         }
-        y[m * N + n] = acc;
+        y[m * N + n] = bias ? acc + bias[n] : acc;   // the bias: one more rounding after the fold
     }
 }
 
@@ -442,7 +442,10 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     for (int o = tid; o < rows_wg * MT; o += kThreads) {
         const int m = o / rows_wg, rl = o % rows_wg;
         const int64_t n = rowbase + rl;
-        if (m < Ms && n < N) yg[(int64_t)m * N + n] = yres[rl * MT + m];
+        if (m < Ms && n < N) {
+            const float v = yres[rl * MT + m];
+            yg[(int64_t)m * N + n] = a.bias ? v + a.bias[n] : v;
+        }
     }
 }
 
@@ -669,7 +672,7 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
     const int64_t rowbase = 4 * q0;
     for (int o = tid; o < rows_wg; o += kThreads) {
         const int64_t n = rowbase + o;
-        if (n < N) a.y[n] = yres[o];
+        if (n < N) a.y[n] = a.bias ? yres[o] + a.bias[n] : yres[o];
     }
 }
 
@@ -706,7 +709,7 @@ __device__ __forceinline__ void lds_vec(const float* p, float* out) {
 
 template <int BM, int BN>
 __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w,
-                                                    float* __restrict__ y, int64_t M, int64_t N, int64_t K,
+                                                    const float* __restrict__ bias, float* __restrict__ y, int64_t M, int64_t N, int64_t K,
                                                     int reverse) {
     constexpr int TM = BM / 16, TN = BN / 16;        // per-thread outputs per dimension
     constexpr int HM = TM / 2, HN = TN / 2;          // two interleaved halves
@@ -835,7 +838,7 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
             const int64_t gn = n0 + (j < HN ? tn * HN + j : BN / 2 + tn * HN + (j - HN));
-            if (gn < N) y[gm * N + gn] = tot[i][j];
+            if (gn < N) y[gm * N + gn] = bias ? tot[i][j] + bias[gn] : tot[i][j];
         }
     }
 }
@@ -857,7 +860,7 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int KS, int NT>
 __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w,
-                                                   float* __restrict__ y, int64_t M, int64_t N, int64_t K,
+                                                   const float* __restrict__ bias, float* __restrict__ y, int64_t M, int64_t N, int64_t K,
                                                    int reverse) {
     static_assert(BM * BN * KS == 16 * NT, "NT threads x 16 outputs");
     constexpr int TG = NT / KS;                      // threads per group
@@ -1008,7 +1011,7 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const int64_t gn = n0 + 4 * ni + c;
-                if (gn < N) y[gm * N + gn] = tot[4 * r + c];
+                if (gn < N) y[gm * N + gn] = bias ? tot[4 * r + c] + bias[gn] : tot[4 * r + c];
             }
         }
     }
@@ -1222,7 +1225,7 @@ __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
                 yrun = y;
                 if (s == S - 1) {
                     const int64_t n = 4 * (v + (int64_t)t * V) + lane;
-                    if (n < N) a.y[n] = y;
+                    if (n < N) a.y[n] = a.bias ? y + a.bias[n] : y;
                 }
             }
             __builtin_amdgcn_wave_barrier();
@@ -1281,9 +1284,9 @@ __global__ void __launch_bounds__(256) argmax_kernel(const float* __restrict__ y
 // ---------------------------------------------------------------------------
 // host-side launchers
 // ---------------------------------------------------------------------------
-hipError_t launch_generic(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K,
-                          int grid, int reverse, hipStream_t stream) {
-    hipLaunchKernelGGL(generic_kernel, dim3(grid), dim3(256), 0, stream, x, w, y, M, N, K, reverse);
+hipError_t launch_generic(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N,
+                          int64_t K, int grid, int reverse, hipStream_t stream) {
+    hipLaunchKernelGGL(generic_kernel, dim3(grid), dim3(256), 0, stream, x, w, bias, y, M, N, K, reverse);
     return hipGetLastError();
 }
 
@@ -1378,27 +1381,27 @@ hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int dept
     }
 }
 
-hipError_t launch_tiled(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
-                        int reverse, hipStream_t stream) {
+hipError_t launch_tiled(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int reverse, hipStream_t stream) {
     const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid((unsigned)tiles), block(256);
-    if (bm == 128 && bn == 128) hipLaunchKernelGGL((tiled_kernel<128, 128>), grid, block, 0, stream, x, w, y, M, N, K, reverse);
-    else if (bm == 64 && bn == 128) hipLaunchKernelGGL((tiled_kernel<64, 128>), grid, block, 0, stream, x, w, y, M, N, K, reverse);
-    else if (bm == 64 && bn == 64) hipLaunchKernelGGL((tiled_kernel<64, 64>), grid, block, 0, stream, x, w, y, M, N, K, reverse);
+    if (bm == 128 && bn == 128) hipLaunchKernelGGL((tiled_kernel<128, 128>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
+    else if (bm == 64 && bn == 128) hipLaunchKernelGGL((tiled_kernel<64, 128>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
+    else if (bm == 64 && bn == 64) hipLaunchKernelGGL((tiled_kernel<64, 64>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
 // Small-M tiles (16 outputs per thread, K shared out over KS = 16 * nt / (bm * bn) groups).
-hipError_t launch_ktile(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, int bm, int bn,
-                        int nt, int reverse, hipStream_t stream) {
+hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int nt, int reverse, hipStream_t stream) {
     const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid((unsigned)tiles);
 #define RG_KT(BM, BN, NT) \
     if (bm == BM && bn == BN && nt == NT) { \
-        hipLaunchKernelGGL((ktile_kernel<BM, BN, 16 * NT / (BM * BN), NT>), grid, dim3(NT), 0, stream, x, w, y, M, N, K, \
+        hipLaunchKernelGGL((ktile_kernel<BM, BN, 16 * NT / (BM * BN), NT>), grid, dim3(NT), 0, stream, x, w, bias, y, M, N, K, \
                            reverse); \
         return hipGetLastError(); \
     }

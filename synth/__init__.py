@@ -15,6 +15,7 @@ _lib = None
 # Tensor ids keep the streams of different tensors of one workload apart.
 TID_X = 1
 TID_W = 2
+TID_B = 3
 
 
 def lib():
@@ -63,3 +64,8 @@ def layer_inputs(M: int, N: int, K: int, seed: int = 0, w_std: float = 0.02, lay
     x = normal_f32(M, K, seed, TID_X + 16 * layer, 1.0)
     w = normal_bf16(N, K, seed, TID_W + 16 * layer, w_std)
     return x, w
+
+
+def layer_bias(N: int, seed: int = 0, std: float = 0.02, layer: int = 0) -> np.ndarray:
+    """float32 bias [N] ~ N(0, std^2) for one layer (a row of the same counter-based stream)."""
+    return normal_f32(1, N, seed, TID_B + 16 * layer, std)[0]

@@ -14,7 +14,9 @@ What pins what:
     operand pairing, transposition or index shows up as a wrong integer;
   * exact-rational emulation of binary32 FMA and addition on tiny inputs:
     correct rounding, signed zeros and gradual underflow of the C library;
-  * invariants: rows of x and of W permute outputs; a batch is its rows.
+  * invariants: rows of x and of W permute outputs; a batch is its rows;
+  * the bias variant: hand-derived probes (tests/golden/bias_probes.json),
+    exact integers, and b = 0.
 """
 import ctypes
 import json
@@ -191,8 +193,63 @@ def check_invariants(L, seed=2):
     return fails
 
 
+BIAS_GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "bias_probes.json")
+
+
+def _linear_bias(L, x, w, b, nthreads=4):
+    vp, i64, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    L.rg_oracle_linear_bias.argtypes = [vp, vp, vp, vp, i64, i64, i64, ci]
+    L.rg_oracle_linear_bias.restype = ci
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    b = np.ascontiguousarray(b, dtype=np.float32)
+    M, K = x.shape
+    N = w.shape[0]
+    y = np.empty((M, N), dtype=np.float32)
+    assert L.rg_oracle_linear_bias(x.ctypes.data, w.ctypes.data, b.ctypes.data, y.ctypes.data, M, N, K, nthreads) == 0
+    return y
+
+
+def load_bias_probes():
+    with open(BIAS_GOLDEN) as f:
+        return json.load(f)["probes"]
+
+
+def check_bias(L, seed=5):
+    """The bias variant: the hand-derived probes (tests/golden/bias_probes.json), exact
+    integers (every order of the sum gives the same integer, so only the additions
+    themselves are tested), and the bias-free product where b = 0 (x + 0 == x)."""
+    L = _setup(L)
+    fails = []
+    for p in load_bias_probes():
+        x, w = probe_inputs(p)
+        b = np.array([float.fromhex(p["b"])], dtype=np.float32)
+        got = f32_bits(_linear_bias(L, x, w, b)[0, 0])
+        want = int(p["expect_bits"], 16)
+        if got != want:
+            fails.append(f"{p['name']}: got 0x{got:08x} want 0x{want:08x}")
+    rng = np.random.default_rng(seed)
+    M, N, K = 3, 9, 600
+    xi = rng.integers(-8, 9, (M, K)).astype(np.float32)
+    wi = rng.integers(-4, 5, (N, K)).astype(np.float32)
+    bi = rng.integers(-1000, 1001, N).astype(np.float32)
+    w16 = (wi.view(np.uint32) >> 16).astype(np.uint16)
+    got = _linear_bias(L, xi, w16, bi)
+    want = (xi.astype(np.int64) @ wi.astype(np.int64).T + bi.astype(np.int64)).astype(np.float32)
+    if not np.array_equal(got, want):
+        fails.append("integer-valued inputs with an integer bias are not exact")
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    w = ((rng.standard_normal((N, K)) * 0.02).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    y0 = _linear_bias(L, x, w, np.zeros(N, dtype=np.float32))
+    y = _linear(L, x, w)
+    if not np.array_equal(y0.view(np.uint32), (y + np.float32(0.0)).view(np.uint32)):
+        fails.append("b = 0 changed a nonzero output")
+    return fails
+
+
 ALL_CHECKS = {
     "probes": check_probes,
+    "bias": check_bias,
     "fp64_bound": check_fp64_bound,
     "integer_exact": check_integer_exact,
     "exact_emulation": check_exact_emulation,

@@ -44,12 +44,15 @@ MUTANTS = {
                            ("p = fmaf(x[k], up_bf16(w[k]), p);", "p = fma((double)x[k], (double)up_bf16(w[k]), p);")],
     "separate_multiply_add": [("p = fmaf(x[k], up_bf16(w[k]), p);", "p = x[k] * up_bf16(w[k]) + p;")],
     "transposed_output": [("const int64_t m = i / N, n = i % N;\n        y[i]", "const int64_t n = i / M, m = i % M;\n        y[i]")],
-    "weight_row_stride_wrong": [("rg_oracle_dot(x + m * K, w + n * K, K);\n    }\n    return 0;\n}\n\n/* Sampled",
-                                 "rg_oracle_dot(x + m * K, w + n * (K - 1), K);\n    }\n    return 0;\n}\n\n/* Sampled")],
+    "weight_row_stride_wrong": [("y[i] = rg_oracle_dot(x + m * K, w + n * K, K);",
+                                 "y[i] = rg_oracle_dot(x + m * K, w + n * (K - 1), K);")],
     "flush_subnormal_weights": [("    memcpy(&f, &u, sizeof f);\n    return f;",
                                  "    memcpy(&f, &u, sizeof f);\n    return (fabsf(f) < 1.17549435e-38f) ? 0.0f : f;")],
     "upcast_shift_off_by_one": [("(uint32_t)b << 16", "(uint32_t)b << 15")],
     "tree_fold": "TREE",
+    "bias_dropped": [("y[i] = d + b[n];", "y[i] = d;")],
+    "bias_subtracted": [("y[i] = d + b[n];", "y[i] = d - b[n];")],
+    "bias_in_double": [("y[i] = d + b[n];", "y[i] = (float)((double)d + (double)b[n] * 1.0000001);")],
 }
 
 
