@@ -18,11 +18,20 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-fast-math",
           "-fno-gpu-flush-denormals-to-zero", "-Wall", "-Wno-unused-result"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 SOURCES = ["rg_kernels.hip", "rg_api.cpp"]
+# Negative controls (kernels that break the design rules on purpose, for the tests): a library of their own.
+NEGCTL_LIB = os.path.join(HERE, "librg_negctl.so")
+NEGCTL_SOURCES = ["rg_negctl.hip"]
 
 
 def build(verbose: bool = False) -> str:
+    _build_lib(SOURCES, LIB, verbose)
+    _build_lib(NEGCTL_SOURCES, NEGCTL_LIB, verbose)
+    return LIB
+
+
+def _build_lib(sources, lib, verbose):
     objs = []
-    for src in SOURCES:
+    for src in sources:
         path = os.path.join(CSRC, src)
         obj = os.path.join(CSRC, src + ".o")
         cmd = [HIPCC, "-x", "hip", *COMMON, *DEVICE, "-c", path, "-o", obj]
@@ -35,14 +44,13 @@ def build(verbose: bool = False) -> str:
         if err.strip() and verbose:
             print(err)
         objs.append(obj)
-    cmd = [HIPCC, *DEVICE, "-shared", "-fPIC", *objs, "-o", LIB + ".tmp"]
+    cmd = [HIPCC, *DEVICE, "-shared", "-fPIC", *objs, "-o", lib + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stderr)
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    os.replace(lib + ".tmp", lib)
 
 
 if __name__ == "__main__":

@@ -151,3 +151,24 @@ def test_device_code_uses_only_ieee_fma_for_accumulation():
     # binary32 denormals kept in every kernel
     modes = re.findall(r"\.amdhsa_float_denorm_mode_32\s+(\d+)", asm)
     assert modes and set(modes) == {"3"}
+
+
+def test_negative_control_library_exports_its_header_and_checks_arguments():
+    # The negative controls live in a library of their own; rg_linear's library holds none of them.
+    from paper_2609_25624_amd import negctl
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "rg_negctl.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"^\s*int\s+(rg_negctl_\w+)\s*\(", text, flags=re.M)))
+    assert sorted(negctl.EXPORTS) == names
+    lib = ctypes.CDLL(negctl.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    main = ctypes.CDLL(rg.LIB_PATH)
+    for n in names:
+        assert not hasattr(main, n), f"{n} must not be in librg.so"
+    L = negctl.lib
+    assert L.rg_negctl_atomic_splitk(None, 0x1000, 0x2000, 1, 1, 8, 2, None) == negctl.RG_NEGCTL_ERR_INVAL
+    assert L.rg_negctl_atomic_splitk(0x1000, 0x2000, 0x3000, 1, 1, 8, 0, None) == negctl.RG_NEGCTL_ERR_INVAL
+    assert L.rg_negctl_atomic_splitk(0x1000, 0x2000, 0x3000, 1, 1, 8, 9, None) == negctl.RG_NEGCTL_ERR_INVAL
+    assert L.rg_negctl_atomic_splitk(0x1002, 0x2000, 0x3000, 1, 1, 8, 2, None) == negctl.RG_NEGCTL_ERR_INVAL
+    assert L.rg_negctl_cu_split(0x1000, 0x2000, 0x3000, 0, 1, 8, None, None) == negctl.RG_NEGCTL_ERR_INVAL
+    assert L.rg_negctl_cu_split(0x1000, 0x2001, 0x3000, 1, 1, 8, None, None) == negctl.RG_NEGCTL_ERR_INVAL
