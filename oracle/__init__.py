@@ -30,6 +30,10 @@ def lib():
         L.rg_oracle_linear.restype = ci
         L.rg_oracle_linear_bias.argtypes = [vp, vp, vp, vp, i64, i64, i64, ci]
         L.rg_oracle_linear_bias.restype = ci
+        L.rg_oracle_linear_f32w.argtypes = [vp, vp, vp, i64, i64, i64, ci]
+        L.rg_oracle_linear_f32w.restype = ci
+        L.rg_ref_fp64_f32w.argtypes = [vp, vp, vp, vp, i64, i64, i64, ci]
+        L.rg_ref_fp64_f32w.restype = ci
         L.rg_oracle_linear_sampled.argtypes = [vp, vp, i64, vp, vp, i64, vp, ci]
         L.rg_oracle_linear_sampled.restype = ci
         L.rg_ref_fp64.argtypes = [vp, vp, vp, vp, i64, i64, i64, ci]
@@ -65,6 +69,23 @@ def linear(x, w, nthreads=None) -> np.ndarray:
     rc = lib().rg_oracle_linear(x.ctypes.data, w.ctypes.data, y.ctypes.data, M, N, K, _threads(nthreads))
     if rc != 0:
         raise ValueError("rg_oracle_linear rejected its arguments")
+    return y
+
+
+def linear_f32w(x, w, nthreads=None) -> np.ndarray:
+    """y[M,N] in the documented order with float32 weights w [N,K] used as they are."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    w = np.ascontiguousarray(w)
+    if w.dtype != np.float32:
+        raise TypeError("w must be float32")
+    if x.ndim != 2 or w.ndim != 2 or x.shape[1] != w.shape[1]:
+        raise ValueError(f"shape mismatch x{x.shape} w{w.shape}")
+    M, K = x.shape
+    N = w.shape[0]
+    y = np.empty((M, N), dtype=np.float32)
+    rc = lib().rg_oracle_linear_f32w(x.ctypes.data, w.ctypes.data, y.ctypes.data, M, N, K, _threads(nthreads))
+    if rc != 0:
+        raise ValueError("rg_oracle_linear_f32w rejected its arguments")
     return y
 
 

@@ -23,6 +23,10 @@
  * binary32 addition after the last segment (Design, eq. 2's "+ b"; the bias
  * never enters a segment chain).
  *
+ * With FP32 weights (rg_oracle_linear_f32w; the paper probes BF16 and FP32
+ * weights alike, Supplement C): the same segments, chains and fold, with the
+ * weight read as the float it is in place of up(W[n,k]).
+ *
  * Nothing depends on m, n or M (batch invariance by construction, rule R4).
  * Arithmetic is IEEE-754 binary32, round to nearest even, gradual underflow:
  * this file is compiled with -ffp-contract=off and without fast-math, and
@@ -87,6 +91,55 @@ int rg_oracle_linear_bias(const float* x, const uint16_t* w, const float* b, flo
         const int64_t m = i / N, n = i % N;
         const float d = rg_oracle_dot(x + m * K, w + n * K, K);
         y[i] = d + b[n];
+    }
+    return 0;
+}
+
+/* One output with FP32 weights: rg_oracle_dot's order, w[k] used as it is. */
+float rg_oracle_dot_f32w(const float* x, const float* w, int64_t K) {
+    float y = 0.0f;
+    int64_t j = 0;
+    for (int64_t k0 = 0; k0 < K; k0 += RG_ORACLE_CHUNK, ++j) {
+        const int64_t k1 = (k0 + RG_ORACLE_CHUNK < K) ? k0 + RG_ORACLE_CHUNK : K;
+        float p = +0.0f;
+        for (int64_t k = k0; k < k1; ++k) p = fmaf(x[k], w[k], p);
+        if (j == 0)
+            y = p;
+        else
+            y = y + p;
+    }
+    return y;
+}
+
+/* y[M][N] for x[M][K] and W[N][K], both float32, row-major. */
+int rg_oracle_linear_f32w(const float* x, const float* w, float* y, int64_t M, int64_t N, int64_t K,
+                          int nthreads) {
+    if (M < 0 || N < 0 || K < 1) return -1;
+    const int64_t total = M * N;
+#pragma omp parallel for schedule(dynamic, 64) num_threads(nthreads > 0 ? nthreads : 1)
+    for (int64_t i = 0; i < total; ++i) {
+        const int64_t m = i / N, n = i % N;
+        y[i] = rg_oracle_dot_f32w(x + m * K, w + n * K, K);
+    }
+    return 0;
+}
+
+/* FP64 reference with FP32 weights: y64 = sum_k (double)x*(double)w, s = sum_k |x*w|. */
+int rg_ref_fp64_f32w(const float* x, const float* w, double* y64, double* abs_sum, int64_t M, int64_t N,
+                     int64_t K, int nthreads) {
+    if (M < 0 || N < 0 || K < 1) return -1;
+    const int64_t total = M * N;
+#pragma omp parallel for schedule(dynamic, 64) num_threads(nthreads > 0 ? nthreads : 1)
+    for (int64_t i = 0; i < total; ++i) {
+        const int64_t m = i / N, n = i % N;
+        double acc = 0.0, s = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+            const double t = (double)x[m * K + k] * (double)w[n * K + k];
+            acc += t;
+            s += fabs(t);
+        }
+        y64[i] = acc;
+        abs_sum[i] = s;
     }
     return 0;
 }

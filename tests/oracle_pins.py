@@ -16,7 +16,11 @@ What pins what:
     correct rounding, signed zeros and gradual underflow of the C library;
   * invariants: rows of x and of W permute outputs; a batch is its rows;
   * the bias variant: hand-derived probes (tests/golden/bias_probes.json),
-    exact integers, and b = 0.
+    exact integers, and b = 0;
+  * FP32 weights: hand-derived probes (tests/golden/f32w_probes.json), the
+    order probes with widened weights, exact emulation, the binary64 bound,
+    integers beyond bfloat16 precision, and agreement with the BF16 path on
+    widened BF16 weights.
 """
 import ctypes
 import json
@@ -247,9 +251,111 @@ def check_bias(L, seed=5):
     return fails
 
 
+F32W_GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "f32w_probes.json")
+
+
+def _linear_f32w(L, x, w, nthreads=4):
+    vp, i64, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    L.rg_oracle_linear_f32w.argtypes = [vp, vp, vp, i64, i64, i64, ci]
+    L.rg_oracle_linear_f32w.restype = ci
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    M, K = x.shape
+    N = w.shape[0]
+    y = np.empty((M, N), dtype=np.float32)
+    assert L.rg_oracle_linear_f32w(x.ctypes.data, w.ctypes.data, y.ctypes.data, M, N, K, nthreads) == 0
+    return y
+
+
+def load_f32w_probes():
+    with open(F32W_GOLDEN) as f:
+        return json.load(f)["probes"]
+
+
+def f32w_probe_inputs(p):
+    K = p["K"]
+    x = np.zeros((1, K), dtype=np.float32)
+    w = np.ones((1, K), dtype=np.float32)
+    for a, b, v in p["x"]:
+        x[0, a:b] = float.fromhex(v)
+    wb = w.view(np.uint32)
+    for a, b, v in p.get("w", []):
+        wb[0, a:b] = int(v, 16)
+    return x, w
+
+
+def emulated_dot_f32w(xr, wr):
+    """The documented order on exact rationals with float32 weights used as they are."""
+    K = len(xr)
+    y = None
+    for k0 in range(0, K, CHUNK):
+        p = 0.0
+        for k in range(k0, min(k0 + CHUNK, K)):
+            p = fx.fma(float(xr[k]), float(wr[k]), p)
+        y = p if y is None else fx.add(y, p)
+    return y
+
+
+def check_f32w(L, seed=6):
+    """FP32 weights: the FP32-weight probes (tests/golden/f32w_probes.json); every
+    BF16 order probe with its weights widened to float32 (the same bits); exact
+    rational emulation with full-precision weights; the binary64 bound; integer
+    weights that bfloat16 cannot hold; and equality with the BF16 oracle when
+    the weights are widened BF16 values."""
+    fails = []
+    for p in load_f32w_probes():
+        x, w = f32w_probe_inputs(p)
+        got = f32_bits(_linear_f32w(L, x, w)[0, 0])
+        if got != int(p["expect_bits"], 16):
+            fails.append(f"{p['name']}: got 0x{got:08x} want {p['expect_bits']}")
+    for p in load_probes():
+        x, wb = probe_inputs(p)
+        w = (wb.astype(np.uint32) << 16).view(np.float32)
+        got = f32_bits(_linear_f32w(L, x, w)[0, 0])
+        if got != int(p["expect_bits"], 16):
+            fails.append(f"{p['name']} with float32 weights: got 0x{got:08x} want {p['expect_bits']}")
+    rng = np.random.default_rng(seed)
+    for K in (1, 17, 256, 257, 520):
+        x = rng.standard_normal((1, K)).astype(np.float32)
+        w = (rng.standard_normal((1, K)) * 0.02).astype(np.float32)
+        got = f32_bits(_linear_f32w(L, x, w)[0, 0])
+        want = f32_bits(emulated_dot_f32w(x[0], w[0]))
+        if got != want:
+            fails.append(f"emulation K={K}: got 0x{got:08x} want 0x{want:08x}")
+    K = 300
+    x = (rng.standard_normal((1, K)) * 2.0 ** rng.integers(-70, 40, K)).astype(np.float32)
+    w = (rng.standard_normal((1, K)) * 2.0 ** rng.integers(-120, 10, K)).astype(np.float32)
+    if f32_bits(_linear_f32w(L, x, w)[0, 0]) != f32_bits(emulated_dot_f32w(x[0], w[0])):
+        fails.append("emulation, wide range with subnormal weights")
+    for K in (7, 255, 256, 257, 513, 1500, 4100):
+        M, N = 2, 3
+        x = rng.standard_normal((M, K)).astype(np.float32)
+        w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+        y = _linear_f32w(L, x, w).astype(np.float64)
+        prod = x.astype(np.float64)[:, None, :] * w.astype(np.float64)[None, :, :]
+        a = np.abs(prod).sum(axis=2)
+        g64 = K * 2.0 ** -53 / (1 - K * 2.0 ** -53)
+        if not np.all(np.abs(y - prod.sum(axis=2)) <= (gamma(K) + g64) * a):
+            fails.append(f"binary64 bound K={K}")
+    M, N, K = 3, 5, 1000
+    xi = rng.integers(-3, 4, (M, K))
+    wi = rng.integers(-300, 301, (N, K))        # most need more than bfloat16's 8 significant bits
+    got = _linear_f32w(L, xi.astype(np.float32), wi.astype(np.float32))
+    if not np.array_equal(got.astype(np.int64), xi @ wi.T) or not np.all(got == xi @ wi.T):
+        fails.append("integer weights beyond bfloat16 precision are not exact")
+    x = rng.standard_normal((4, 700)).astype(np.float32)
+    wb = ((rng.standard_normal((6, 700)) * 0.02).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    y16 = _linear(_setup(L), x, wb)
+    y32 = _linear_f32w(L, x, (wb.astype(np.uint32) << 16).view(np.float32))
+    if not np.array_equal(y16.view(np.uint32), y32.view(np.uint32)):
+        fails.append("widened BF16 weights as float32 differ from the BF16 path")
+    return fails
+
+
 ALL_CHECKS = {
     "probes": check_probes,
     "bias": check_bias,
+    "f32w": check_f32w,
     "fp64_bound": check_fp64_bound,
     "integer_exact": check_integer_exact,
     "exact_emulation": check_exact_emulation,

@@ -53,6 +53,11 @@ MUTANTS = {
     "bias_dropped": [("y[i] = d + b[n];", "y[i] = d;")],
     "bias_subtracted": [("y[i] = d + b[n];", "y[i] = d - b[n];")],
     "bias_in_double": [("y[i] = d + b[n];", "y[i] = (float)((double)d + (double)b[n] * 1.0000001);")],
+    "f32w_weight_truncated_to_bf16": [("p = fmaf(x[k], w[k], p);", "p = fmaf(x[k], up_bf16((uint16_t)(f32_bits_of(w[k]) >> 16)), p);"),
+                                      ("/* One output with FP32 weights", "static uint32_t f32_bits_of(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }\n/* One output with FP32 weights")],
+    "f32w_flush_subnormal_weights": [("p = fmaf(x[k], w[k], p);", "p = fmaf(x[k], (fabsf(w[k]) < 1.17549435e-38f) ? 0.0f : w[k], p);")],
+    "f32w_segment_512": [("const int64_t k1 = (k0 + RG_ORACLE_CHUNK < K) ? k0 + RG_ORACLE_CHUNK : K;\n        float p = +0.0f;\n        for (int64_t k = k0; k < k1; ++k) p = fmaf(x[k], w[k], p);",
+                          "const int64_t k1 = (k0 + 2 * RG_ORACLE_CHUNK < K) ? k0 + 2 * RG_ORACLE_CHUNK : K;\n        float p = +0.0f;\n        for (int64_t k = k0; k < k1; ++k) p = fmaf(x[k], w[k], p);\n        k0 += RG_ORACLE_CHUNK;")],
 }
 
 
