@@ -154,6 +154,73 @@ def run_configs():
             "rotated_copies": nrot}), flush=True)
         del xd, ws, w0, y
         torch.cuda.empty_cache()
+    run_variant_configs()
+
+
+# The NEXT-row variants, timed the same way: FP32 weights (rg_linear_f32w; weight
+# bytes 4NK) and the bias epilogue (rg_linear_bias) on the 8B-shaped layers.
+VARIANT_CONFIGS = [(v, name, M, N, K) for v in ("f32w", "bias") for M in (1, 4, 16)
+                   for (name, N, K) in (("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
+                                        ("down", 4096, 14336)) if v == "f32w" or M == 1]
+
+
+def run_variant_configs():
+    import numpy as np
+    import torch
+
+    import oracle
+    import synth
+    import paper_2609_25624_amd as rg
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    for variant, name, M, N, K in VARIANT_CONFIGS:
+        layer = hash(name) % 97
+        x = synth.normal_f32(M, K, 0, 1 + 16 * layer, 1.0)
+        xd = torch.from_numpy(x).to(dev)
+        if variant == "f32w":
+            w = synth.normal_f32(N, K, 0, 5 + 16 * layer, 0.02)
+            wbytes = 4.0 * N * K
+            w0 = torch.from_numpy(w).to(dev)
+            call = lambda wt, y: rg.rg_linear_f32w(xd, wt, y, stream=stream)
+            plan = rg.rg_plan_f32w(M, N, K)
+        else:
+            w = synth.normal_bf16(N, K, 0, 2 + 16 * layer, 0.02)
+            b = synth.layer_bias(N, seed=0, layer=layer)
+            bd = torch.from_numpy(b).to(dev)
+            wbytes = 2.0 * N * K
+            w0 = torch.from_numpy(w.view(np.int16)).to(dev)
+            call = lambda wt, y: rg.rg_linear_bias(xd, wt, bd, y, stream=stream)
+            plan = rg.rg_plan(M, N, K)
+        nrot = max(1, int(np.ceil(ROTATE_BYTES / wbytes)))
+        ws = [w0] + [w0.clone() for _ in range(nrot - 1)]
+        y = torch.empty((M, N), dtype=torch.float32, device=dev)
+        R = 200
+        for i in range(5):
+            call(ws[i % nrot], y)
+        loops = []
+        for rep in range(5):
+            a = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for i in range(R):
+                call(ws[i % nrot], y)
+            e.record(stream)
+            torch.cuda.synchronize()
+            loops.append(a.elapsed_time(e) * 1e3 / R)
+        us = sorted(loops)[2]
+        call(ws[0], y)
+        torch.cuda.synchronize()
+        got = y.cpu().numpy()
+        want = oracle.linear_f32w(x, w) if variant == "f32w" else oracle.linear_bias(x, w, b)
+        exact = bool(np.array_equal(got.view(np.uint32), want.view(np.uint32)))
+        print(json.dumps({
+            "variant": variant, "layer": name, "M": M, "N": N, "K": K, "us_per_call": round(us, 3),
+            "weight_bytes": int(wbytes), "weight_TBs": round(wbytes / (us * 1e-6) / 1e12, 4),
+            "frac_of_8TBs": round(wbytes / (us * 1e-6) / (HBM_PEAK_GBS * 1e9), 4),
+            "bitexact": exact, "checked": "all", "kernel": plan["kernel_name"], "grid_wgs": plan["grid_wgs"],
+            "rotated_copies": nrot}), flush=True)
+        del xd, ws, w0, y
+        torch.cuda.empty_cache()
 
 
 def _csv_rows(path):

@@ -58,7 +58,7 @@ extern "C" {
 typedef enum {
     RG_OK = 0,
     RG_ERR_INVAL = 1,    /* null pointer, M/N/K < 1, or M*K, N*K, M*N overflow int64 */
-    RG_ERR_ALIGN = 2,    /* x, W or y not 4-byte aligned (W: 2-byte) */
+    RG_ERR_ALIGN = 2,    /* x, W or y not 4-byte aligned (BF16 W: 2-byte) */
     RG_ERR_ARCH = 3,     /* current device is not gfx950 */
     RG_ERR_HIP = 4,      /* a HIP runtime call failed (launch or query) */
     RG_ERR_RANGE = 5,    /* an rg_launch_t field is out of its documented range */
@@ -72,8 +72,10 @@ typedef enum {
     RG_KERNEL_TILED = 2,     /* larger M: register-tiled kernel, whole K per workgroup */
     RG_KERNEL_DECODE_XS = 3, /* M == 1: streaming GEMV with x streamed through LDS beside W */
     RG_KERNEL_GEMV = 4,      /* M == 1, K % 256 == 0, K >= 4096: 32 KB W bursts, whole rows per wave */
+    RG_KERNEL_F32W_STREAM = 5, /* FP32 weights only (rg_linear_f32w), M <= 4: 8-row blocks streamed
+                                  through LDS, one chain per lane */
     RG_KERNEL_KTILE = 6      /* 4 < M <= 64 (any M when forced): 4 x 4 register tiles, K segments
-                                shared out over thread groups (id 5 is not used) */
+                                shared out over thread groups */
 } rg_kernel_id;
 
 /* Scheduling overrides for the determinism tests.  0 in a field = planner
@@ -140,13 +142,33 @@ int rg_linear(const float* x, const uint16_t* w_bf16, float* y, int64_t M, int64
 int rg_linear_bias(const float* x, const uint16_t* w_bf16, const float* bias, float* y, int64_t M, int64_t N,
                    int64_t K, void* stream);
 
+/*
+ * y = x * W^T with FP32 weights, in RG-ORDER-1 with the weight used as it is in
+ * place of up(W) (paper: Supplement C probes BF16 and FP32 weights alike; the
+ * same segments, chains and ascending fold, so FP32 weights that hold widened
+ * BF16 values give rg_linear's bits exactly).
+ *   x      device pointer, float32 [M][K], 4-byte aligned
+ *   w_f32  device pointer, float32 [N][K], 4-byte aligned
+ *   y      device pointer, float32 [M][N], 4-byte aligned, must not overlap x or W
+ * Kernels: RG_KERNEL_F32W_STREAM for M <= 4, then ktile (M <= 64) and tiled,
+ * all needing 16-byte aligned x and W and K % 4 == 0; other shapes take the
+ * generic kernel.  Errors, streams and ownership as rg_linear; the same
+ * rg_linear_set_launch overrides apply (decode, decode_xs and gemv cannot be
+ * forced here: RG_ERR_RANGE).
+ */
+int rg_linear_f32w(const float* x, const float* w_f32, float* y, int64_t M, int64_t N, int64_t K, void* stream);
+
 /* Set (cfg != NULL) or reset (cfg == NULL) the scheduling overrides used by
- * later rg_linear calls.  RG_ERR_RANGE if a field is out of range. */
+ * later rg_linear, rg_linear_bias and rg_linear_f32w calls.  RG_ERR_RANGE if a
+ * field is out of range. */
 int rg_linear_set_launch(const rg_launch_t* cfg);
 
 /* Fill *out with the plan for (M, N, K) under the current overrides.  A pure
  * function of its arguments and the overrides; queries no device.  CPU safe. */
 int rg_plan(int64_t M, int64_t N, int64_t K, rg_plan_t* out);
+
+/* The same for rg_linear_f32w (FP32 weights). */
+int rg_plan_f32w(int64_t M, int64_t N, int64_t K, rg_plan_t* out);
 
 /* Comparison point only (the scheme the paper improves on, Design, eq. 1):
  * w_f32[n][k] = up(W[n][k]) written to a caller-provided FP32 buffer of N*K

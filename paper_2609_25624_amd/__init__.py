@@ -12,7 +12,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librg.so")
 
 RG_OK, RG_ERR_INVAL, RG_ERR_ALIGN, RG_ERR_ARCH, RG_ERR_HIP, RG_ERR_RANGE, RG_ERR_ALIAS = range(7)
-KERNELS = {0: "generic", 1: "decode", 2: "tiled", 3: "decode_xs", 4: "gemv", 6: "ktile"}
+KERNELS = {0: "generic", 1: "decode", 2: "tiled", 3: "decode_xs", 4: "gemv", 5: "f32w_stream", 6: "ktile"}
 CHUNK = 256
 
 
@@ -52,8 +52,10 @@ def _load():
     sig = {
         "rg_linear": [vp, vp, vp, i64, i64, i64, vp],
         "rg_linear_bias": [vp, vp, vp, vp, i64, i64, i64, vp],
+        "rg_linear_f32w": [vp, vp, vp, i64, i64, i64, vp],
         "rg_linear_set_launch": [ctypes.POINTER(rg_launch_t)],
         "rg_plan": [i64, i64, i64, ctypes.POINTER(rg_plan_t)],
+        "rg_plan_f32w": [i64, i64, i64, ctypes.POINTER(rg_plan_t)],
         "rg_cast_bf16_f32": [vp, vp, i64, vp],
         "rg_argmax_rows": [vp, vp, i64, i64, vp],
         "rg_stream_create_cu_mask": [ctypes.POINTER(ctypes.c_uint32), ctypes.c_uint32, ctypes.POINTER(vp)],
@@ -73,7 +75,8 @@ def _load():
 lib = _load()
 
 # Every symbol include/rg.h declares (checked by the tests).
-EXPORTS = ("rg_linear", "rg_linear_bias", "rg_linear_set_launch", "rg_plan", "rg_cast_bf16_f32", "rg_argmax_rows",
+EXPORTS = ("rg_linear", "rg_linear_bias", "rg_linear_f32w", "rg_linear_set_launch", "rg_plan", "rg_plan_f32w",
+           "rg_cast_bf16_f32", "rg_argmax_rows",
            "rg_stream_create_cu_mask", "rg_stream_destroy", "rg_device_cu_count", "rg_strerror",
            "rg_last_hip_error")
 
@@ -140,6 +143,22 @@ def rg_linear_bias(x, w, b, y, stream=None):
     return y
 
 
+def rg_linear_f32w(x, w, y, stream=None):
+    """y[M,N] = x[M,K] * w[N,K]^T in the fixed order with float32 weights used as they are."""
+    import torch
+    px = _tensor_ptr(x, (torch.float32,), "x")
+    pw = _tensor_ptr(w, (torch.float32,), "w")
+    py = _tensor_ptr(y, (torch.float32,), "y")
+    if x.dim() != 2 or w.dim() != 2 or y.dim() != 2:
+        raise ValueError("x, w, y must be 2-D")
+    M, K = x.shape
+    N = w.shape[0]
+    if w.shape[1] != K or tuple(y.shape) != (M, N):
+        raise ValueError(f"shape mismatch x{tuple(x.shape)} w{tuple(w.shape)} y{tuple(y.shape)}")
+    _check(lib.rg_linear_f32w(px, pw, py, M, N, K, _stream_ptr(stream)), "rg_linear_f32w")
+    return y
+
+
 def rg_linear_ptr(x_ptr, w_ptr, y_ptr, M, N, K, stream_ptr=0):
     """Raw-pointer form of rg_linear (device pointers as integers)."""
     _check(lib.rg_linear(x_ptr, w_ptr, y_ptr, M, N, K, stream_ptr), "rg_linear")
@@ -153,7 +172,7 @@ def rg_linear_set_launch(cfg=None, **kw):
     c = rg_launch_t()
     for k, v in dict(cfg or {}, **kw).items():
         if k == "kernel" and isinstance(v, str):
-            v = {"generic": 1, "decode": 2, "tiled": 3, "decode_xs": 4, "gemv": 5, "ktile": 7}[v]
+            v = {"generic": 1, "decode": 2, "tiled": 3, "decode_xs": 4, "gemv": 5, "f32w_stream": 6, "ktile": 7}[v]
         setattr(c, k, int(v))
     _check(lib.rg_linear_set_launch(ctypes.byref(c)), "rg_linear_set_launch")
 
@@ -161,6 +180,14 @@ def rg_linear_set_launch(cfg=None, **kw):
 def rg_plan(M, N, K):
     p = rg_plan_t()
     _check(lib.rg_plan(M, N, K, ctypes.byref(p)), "rg_plan")
+    d = {f: getattr(p, f) for f, _ in rg_plan_t._fields_}
+    d["kernel_name"] = KERNELS.get(d["kernel"], "?")
+    return d
+
+
+def rg_plan_f32w(M, N, K):
+    p = rg_plan_t()
+    _check(lib.rg_plan_f32w(M, N, K, ctypes.byref(p)), "rg_plan_f32w")
     d = {f: getattr(p, f) for f, _ in rg_plan_t._fields_}
     d["kernel_name"] = KERNELS.get(d["kernel"], "?")
     return d

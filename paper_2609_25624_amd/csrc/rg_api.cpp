@@ -213,6 +213,29 @@ bool ktile_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan*
     return true;
 }
 
+// Register-tiled kernel: the largest tile that still gives every CU a few workgroups.
+int tiled_schedule(int64_t M, int64_t N, Plan* p) {
+    const int64_t t128 = ceil_div(M, 128) * ceil_div(N, 128);
+    const int64_t t64x128 = ceil_div(M, 64) * ceil_div(N, 128);
+    if (t128 >= 2 * kNominalCUs) { p->tile_m = 128; p->tile_n = 128; }
+    else if (t64x128 >= kNominalCUs) { p->tile_m = 64; p->tile_n = 128; }
+    else { p->tile_m = 64; p->tile_n = 64; }
+    const int64_t tiles = ceil_div(M, p->tile_m) * ceil_div(N, p->tile_n);
+    if (tiles > 0x7fffffff) return RG_ERR_RANGE;
+    p->grid = (int)tiles;
+    p->nw = 4;
+    return RG_OK;
+}
+
+// One thread per output, grid-strided.
+void generic_schedule(int64_t M, int64_t N, const rg_launch_t& o, Plan* p) {
+    const int64_t blocks = ceil_div(M * N, 256);
+    int64_t grid = o.grid_wgs > 0 ? o.grid_wgs : (blocks < 8 * kNominalCUs ? blocks : 8 * kNominalCUs);
+    if (grid < 1) grid = 1;
+    p->grid = (int)grid;
+    p->nw = 4;
+}
+
 // The planner.  `fast_ok`: x and W 16-byte aligned and K % 8 == 0.
 int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& o, Plan* p) {
     const int64_t J = ceil_div(K, rg::kChunk);
@@ -242,7 +265,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         if (want == RG_KERNEL_TILED && !tiled_ok) return RG_ERR_RANGE;
         if (want == RG_KERNEL_GEMV && !gemv_ok) return RG_ERR_RANGE;
         if (want == RG_KERNEL_KTILE && !fast_ok) return RG_ERR_RANGE;   // any M when forced
-        if (want == 5) return RG_ERR_RANGE;                      // unused kernel id
+        if (want == RG_KERNEL_F32W_STREAM) return RG_ERR_RANGE;   // FP32 weights only
     }
     p->mslices = 1;
     p->kernel = want;
@@ -275,25 +298,45 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
             p->mslices = 1;
         }
     }
-    if (p->kernel == RG_KERNEL_TILED) {
-        // largest tile that still gives every CU a few workgroups
-        const int64_t t128 = ceil_div(M, 128) * ceil_div(N, 128);
-        const int64_t t64x128 = ceil_div(M, 64) * ceil_div(N, 128);
-        if (t128 >= 2 * kNominalCUs) { p->tile_m = 128; p->tile_n = 128; }
-        else if (t64x128 >= kNominalCUs) { p->tile_m = 64; p->tile_n = 128; }
-        else { p->tile_m = 64; p->tile_n = 64; }
-        const int64_t tiles = ceil_div(M, p->tile_m) * ceil_div(N, p->tile_n);
-        if (tiles > 0x7fffffff) return RG_ERR_RANGE;
-        p->grid = (int)tiles;
-        p->nw = 4;
+    if (p->kernel == RG_KERNEL_TILED) return tiled_schedule(M, N, p);
+    if (p->kernel == RG_KERNEL_GENERIC) generic_schedule(M, N, o, p);
+    return RG_OK;
+}
+
+// The planner for FP32 weights (rg_linear_f32w).  `fast_ok`: x and W 16-byte
+// aligned and K % 4 == 0.  M <= 4: the FP32-weight streaming kernel; then the
+// same ktile / tiled / generic kernels as BF16 weights (their weight loads are
+// templated on the element type).
+int make_plan_f32w(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& o, Plan* p) {
+    int want = RG_KERNEL_GENERIC;
+    if (fast_ok && M <= 4) want = RG_KERNEL_F32W_STREAM;
+    else if (fast_ok && M <= kDecodeMaxM) want = RG_KERNEL_KTILE;
+    else if (fast_ok) want = RG_KERNEL_TILED;
+    const bool forced = o.kernel > 0;
+    if (forced) {
+        want = o.kernel - 1;
+        if (want == RG_KERNEL_DECODE || want == RG_KERNEL_DECODE_XS || want == RG_KERNEL_GEMV) return RG_ERR_RANGE;
+        if (want != RG_KERNEL_GENERIC && !fast_ok) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_F32W_STREAM && M > 4) return RG_ERR_RANGE;
     }
-    if (p->kernel == RG_KERNEL_GENERIC) {
-        const int64_t blocks = ceil_div(M * N, 256);
+    p->kernel = want;
+    p->reverse = o.grid_order;
+    p->mslices = 1;
+    if (want == RG_KERNEL_F32W_STREAM) {
+        if ((o.waves_per_wg > 0 && o.waves_per_wg != 4) || o.depth > 0 || o.tile_n > 0) return RG_ERR_RANGE;
+        // 8-row blocks of W; up to 8 workgroups per CU (measured: more workgroups in flight
+        // stream the large layers faster)
+        const int64_t blocks = ceil_div(N, 8);
         int64_t grid = o.grid_wgs > 0 ? o.grid_wgs : (blocks < 8 * kNominalCUs ? blocks : 8 * kNominalCUs);
-        if (grid < 1) grid = 1;
+        p->mt = M <= 1 ? 1 : (M <= 2 ? 2 : 4);
         p->grid = (int)grid;
         p->nw = 4;
+        p->rq = 2;                                    // reported as 8 rows per round
+        return RG_OK;
     }
+    if (want == RG_KERNEL_KTILE) return ktile_schedule(M, N, K, o, p) ? RG_OK : RG_ERR_RANGE;
+    if (want == RG_KERNEL_TILED) return tiled_schedule(M, N, p);
+    generic_schedule(M, N, o, p);
     return RG_OK;
 }
 
@@ -358,6 +401,26 @@ int rg_plan(int64_t M, int64_t N, int64_t K, rg_plan_t* out) {
     if (!mul_ok(M, K) || !mul_ok(N, K) || !mul_ok(M, N)) return RG_ERR_INVAL;
     Plan p;
     const int s = make_plan(M, N, K, (K % 8) == 0, current_launch(), &p);
+    if (s != RG_OK) return s;
+    std::memset(out, 0, sizeof *out);
+    out->order_id = RG_ORDER_ID;
+    out->chunk = rg::kChunk;
+    out->nchunks = ceil_div(K, rg::kChunk);
+    out->kernel = p.kernel;
+    out->waves_per_wg = p.nw;
+    out->grid_wgs = p.grid;
+    out->depth = p.depth;
+    out->rows_per_round = 4 * p.rq;
+    out->tile_m = p.tile_m;
+    out->tile_n = p.tile_n;
+    return RG_OK;
+}
+
+int rg_plan_f32w(int64_t M, int64_t N, int64_t K, rg_plan_t* out) {
+    if (!out || M < 1 || N < 1 || K < 1) return RG_ERR_INVAL;
+    if (!mul_ok(M, K) || !mul_ok(N, K) || !mul_ok(M, N)) return RG_ERR_INVAL;
+    Plan p;
+    const int s = make_plan_f32w(M, N, K, (K % 4) == 0, current_launch(), &p);
     if (s != RG_OK) return s;
     std::memset(out, 0, sizeof *out);
     out->order_id = RG_ORDER_ID;
@@ -446,9 +509,50 @@ int linear_impl(const float* x, const uint16_t* w, const float* bias, float* y, 
     return hip_status(e);
 }
 
+int linear_f32w_impl(const float* x, const float* w, float* y, int64_t M, int64_t N, int64_t K, void* stream) {
+    if (!x || !w || !y || M < 1 || N < 1 || K < 1) return RG_ERR_INVAL;
+    if (!mul_ok(M, K) || !mul_ok(N, K) || !mul_ok(M, N)) return RG_ERR_INVAL;
+    if (((uintptr_t)x & 3) || ((uintptr_t)w & 3) || ((uintptr_t)y & 3)) return RG_ERR_ALIGN;
+    if (overlaps(y, (size_t)(M * N) * 4, x, (size_t)(M * K) * 4) ||
+        overlaps(y, (size_t)(M * N) * 4, w, (size_t)(N * K) * 4))
+        return RG_ERR_ALIAS;
+    const int dc = device_check(nullptr);
+    if (dc != RG_OK) return dc;
+    const bool fast_ok = (K % 4) == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)w & 15) == 0;
+    Plan p;
+    const int s = make_plan_f32w(M, N, K, fast_ok, current_launch(), &p);
+    if (s != RG_OK) return s;
+    hipStream_t st = (hipStream_t)stream;
+    (void)hipGetLastError();
+    hipError_t e = hipSuccess;
+    if (p.kernel == RG_KERNEL_F32W_STREAM) {
+        rg::F32wArgs a;
+        a.x = x;
+        a.w = w;
+        a.y = y;
+        a.M = M;
+        a.N = N;
+        a.K = K;
+        a.J = (int)ceil_div(K, rg::kChunk);
+        a.reverse = p.reverse;
+        e = rg::launch_f32w_stream(a, p.mt, p.grid, st);
+    } else if (p.kernel == RG_KERNEL_KTILE) {
+        e = rg::launch_ktile(x, w, nullptr, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.reverse, st);
+    } else if (p.kernel == RG_KERNEL_TILED) {
+        e = rg::launch_tiled(x, w, nullptr, y, M, N, K, p.tile_m, p.tile_n, p.reverse, st);
+    } else {
+        e = rg::launch_generic(x, w, nullptr, y, M, N, K, p.grid, p.reverse, st);
+    }
+    return hip_status(e);
+}
+
 }  // namespace
 
 extern "C" {
+
+int rg_linear_f32w(const float* x, const float* w, float* y, int64_t M, int64_t N, int64_t K, void* stream) {
+    return linear_f32w_impl(x, w, y, M, N, K, stream);
+}
 
 int rg_linear(const float* x, const uint16_t* w, float* y, int64_t M, int64_t N, int64_t K, void* stream) {
     return linear_impl(x, w, nullptr, y, M, N, K, stream);

@@ -39,14 +39,31 @@ struct GemvArgs {
     int reverse;        // 1: workgroup b takes the quads of workgroup grid-1-b
 };
 
+// FP32-weight streaming kernel (M <= mt <= 4, K % 4 == 0, x and w 16-byte aligned).
+struct F32wArgs {
+    const float* x;
+    const float* w;
+    float* y;
+    int64_t M, N, K;
+    int J;          // ceil(K / kChunk)
+    int reverse;    // reversed workgroup-to-block mapping
+};
+
 hipError_t launch_generic(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N,
                           int64_t K, int grid, int reverse, hipStream_t stream);
+hipError_t launch_generic(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N,
+                          int64_t K, int grid, int reverse, hipStream_t stream);
+hipError_t launch_f32w_stream(const F32wArgs& a, int mt, int grid, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_gemv(const GemvArgs& a, int grid, int nw, hipStream_t stream);
 hipError_t launch_tiled(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
                         int bm, int bn, int reverse, hipStream_t stream);
+hipError_t launch_tiled(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int reverse, hipStream_t stream);
 hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int nt, int reverse, hipStream_t stream);
+hipError_t launch_ktile(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
                         int bm, int bn, int nt, int reverse, hipStream_t stream);
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream);
 hipError_t launch_argmax(const float* y, int64_t* out, int64_t M, int64_t N, hipStream_t stream);

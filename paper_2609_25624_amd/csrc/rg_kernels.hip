@@ -32,6 +32,35 @@ __device__ __forceinline__ float up_lo(uint32_t v) { return __uint_as_float(v <<
 __device__ __forceinline__ float up_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 __device__ __forceinline__ float up1(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
+// Weight element types.  bfloat16 bit patterns are widened exactly (up1 and
+// friends); float32 weights (the FP32-weight variant) are used as they are.
+// A 16-byte vector load carries E elements.
+__device__ __forceinline__ float wval(uint16_t b) { return up1(b); }
+__device__ __forceinline__ float wval(float f) { return f; }
+
+template <typename WT>
+struct WVec;
+template <>
+struct WVec<uint16_t> {
+    using V = uint4;
+    static constexpr int E = 8;
+    static __device__ __forceinline__ V zero() { return make_uint4(0u, 0u, 0u, 0u); }
+    static __device__ __forceinline__ float get(const V& v, int h) {
+        const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+        return (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+    }
+};
+template <>
+struct WVec<float> {
+    using V = float4;
+    static constexpr int E = 4;
+    static __device__ __forceinline__ V zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+    static __device__ __forceinline__ float get(const V& v, int h) {
+        const float d[4] = {v.x, v.y, v.z, v.w};
+        return d[h];
+    }
+};
+
 // Broadcast lane E of every quad (4 lanes) to the whole quad (DPP quad_perm).
 template <int E>
 __device__ __forceinline__ float quad_bcast(float v) {
@@ -138,8 +167,9 @@ __device__ __forceinline__ float fold_partials(const float* p, int J) {
 // ---------------------------------------------------------------------------
 // generic kernel: one thread per output, any K, any alignment.
 // ---------------------------------------------------------------------------
+template <typename WT>
 __global__ void __launch_bounds__(256) generic_kernel(const float* __restrict__ x,
-                                                      const uint16_t* __restrict__ w,
+                                                      const WT* __restrict__ w,
                                                       const float* __restrict__ bias, float* __restrict__ y, int64_t M, int64_t N,
                                                       int64_t K, int reverse) {
     const int64_t total = M * N;
@@ -148,12 +178,12 @@ __global__ void __launch_bounds__(256) generic_kernel(const float* __restrict__ 
     for (int64_t idx = b * blockDim.x + threadIdx.x; idx < total; idx += stride) {
         const int64_t m = idx / N, n = idx % N;
         const float* xr = x + m * K;
-        const uint16_t* wr = w + n * K;
+        const WT* wr = w + n * K;
         float acc = 0.0f;
         for (int64_t k0 = 0, j = 0; k0 < K; k0 += kChunk, ++j) {
             const int64_t k1 = (k0 + kChunk < K) ? k0 + kChunk : K;
             float p = 0.0f;
-            for (int64_t k = k0; k < k1; ++k) p = __builtin_fmaf(xr[k], up1(wr[k]), p);
+            for (int64_t k = k0; k < k1; ++k) p = __builtin_fmaf(xr[k], wval(wr[k]), p);
             acc = (j == 0) ? p : acc + p;
         }
         y[m * N + n] = bias ? acc + bias[n] : acc;   // the bias: one more rounding after the fold
@@ -707,8 +737,8 @@ __device__ __forceinline__ void lds_vec(const float* p, float* out) {
     }
 }
 
-template <int BM, int BN>
-__global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w,
+template <int BM, int BN, typename WT>
+__global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x, const WT* __restrict__ w,
                                                     const float* __restrict__ bias, float* __restrict__ y, int64_t M, int64_t N, int64_t K,
                                                     int reverse) {
     constexpr int TM = BM / 16, TN = BN / 16;        // per-thread outputs per dimension
@@ -724,11 +754,13 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
     const int64_t b = reverse ? (int64_t)(gridDim.x - 1 - blockIdx.x) : (int64_t)blockIdx.x;
     const int64_t m0 = (b / tiles_n) * BM, n0 = (b % tiles_n) * BN;
 
-    // staging roles: x tile BM x 16 floats, W tile BN x 16 bf16
+    // staging roles: x tile BM x 16 floats, W tile BN x 16 weights (16-byte vectors of WE)
+    using WV = WVec<WT>;
+    constexpr int WE = WV::E, WPR = kTK / WE;        // weights per vector, vectors per tile row
     constexpr int XF4 = BM * kTK / 4 / 256;          // float4 loads per thread for x
-    constexpr int WU4 = (BN * kTK / 8 + 255) / 256;  // uint4 (8 bf16) loads per thread for W
+    constexpr int WU4 = (BN * WPR + 255) / 256;      // weight vector loads per thread
     float4 xr[XF4];
-    uint4 wr[WU4];
+    typename WV::V wr[WU4];
 
     auto load_slab = [&](int64_t k0) {
 #pragma unroll
@@ -741,11 +773,11 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
         }
 #pragma unroll
         for (int u = 0; u < WU4; ++u) {
-            const int idx = tid + 256 * u;            // over BN rows x 2 uint4
-            const int row = idx >> 1, kh = idx & 1;
-            const int64_t gn = n0 + row, gk = k0 + 8 * kh;
-            const bool ok = row < BN && gn < N && gk + 8 <= K;
-            wr[u] = ok ? *reinterpret_cast<const uint4*>(w + gn * K + gk) : make_uint4(0u, 0u, 0u, 0u);
+            const int idx = tid + 256 * u;            // over BN rows x WPR vectors
+            const int row = idx / WPR, kh = idx % WPR;
+            const int64_t gn = n0 + row, gk = k0 + WE * kh;
+            const bool ok = row < BN && gn < N && gk + WE <= K;
+            wr[u] = ok ? *reinterpret_cast<const typename WV::V*>(w + gn * K + gk) : WV::zero();
         }
     };
     auto store_slab = [&](int buf) {
@@ -761,11 +793,10 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
 #pragma unroll
         for (int u = 0; u < WU4; ++u) {
             const int idx = tid + 256 * u;
-            const int row = idx >> 1, kh = idx & 1;
+            const int row = idx / WPR, kh = idx % WPR;
             if (row < BN) {
-                const uint32_t d[4] = {wr[u].x, wr[u].y, wr[u].z, wr[u].w};
 #pragma unroll
-                for (int h = 0; h < 8; ++h) ws[buf][8 * kh + h][row] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+                for (int h = 0; h < WE; ++h) ws[buf][WE * kh + h][row] = WV::get(wr[u], h);
             }
         }
     };
@@ -858,8 +889,8 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
 // sum).  Splitting K this way gives small-M shapes enough independent work
 // for several waves per SIMD while the order stays the documented one.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int KS, int NT>
-__global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w,
+template <int BM, int BN, int KS, int NT, typename WT>
+__global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, const WT* __restrict__ w,
                                                    const float* __restrict__ bias, float* __restrict__ y, int64_t M, int64_t N, int64_t K,
                                                    int reverse) {
     static_assert(BM * BN * KS == 16 * NT, "NT threads x 16 outputs");
@@ -867,8 +898,10 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
     constexpr int KT = KS >= 8 ? 8 : 16;             // elements per slab
     constexpr int NSL = kChunk / KT;                 // slabs per segment
     constexpr int PADM = BM + 4, PADN = BN + 4;
+    using WV = WVec<WT>;
+    constexpr int WE = WV::E, WPR = KT / WE;         // weights per vector, vectors per slab row
     constexpr int XPT = (BM * KT / 4 + TG - 1) / TG; // float4 x loads per thread
-    constexpr int WPT = (BN * KT / 8 + TG - 1) / TG; // uint4 W loads per thread
+    constexpr int WPT = (BN * WPR + TG - 1) / TG;    // weight vector loads per thread
     __shared__ __attribute__((aligned(16))) float xs[KS][2][KT][PADM];
     __shared__ __attribute__((aligned(16))) float ws[KS][2][KT][PADN];
     __shared__ __attribute__((aligned(16))) float part[KS > 1 ? KS - 1 : 1][TG][16];
@@ -883,7 +916,7 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
     const int rounds = (J + KS - 1) / KS;
 
     float4 xr[XPT];
-    uint4 wr[WPT];
+    typename WV::V wr[WPT];
     // slab sl of this group's segment in round t
     auto load_slab = [&](int t, int sl) {
         const int64_t j = (int64_t)t * KS + g;
@@ -898,11 +931,11 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
         }
 #pragma unroll
         for (int u = 0; u < WPT; ++u) {
-            const int idx = tg + TG * u;                  // over BN rows x KT/8 uint4
-            const int row = idx / (KT / 8), kh = idx % (KT / 8);
-            const int64_t gn = n0 + row, gk = k0 + 8 * kh;
-            const bool ok = idx < BN * KT / 8 && j < J && gn < N && gk + 8 <= K;
-            wr[u] = ok ? *reinterpret_cast<const uint4*>(w + gn * K + gk) : make_uint4(0u, 0u, 0u, 0u);
+            const int idx = tg + TG * u;                  // over BN rows x WPR vectors
+            const int row = idx / WPR, kh = idx % WPR;
+            const int64_t gn = n0 + row, gk = k0 + WE * kh;
+            const bool ok = idx < BN * WPR && j < J && gn < N && gk + WE <= K;
+            wr[u] = ok ? *reinterpret_cast<const typename WV::V*>(w + gn * K + gk) : WV::zero();
         }
     };
     auto store_slab = [&](int buf) {
@@ -920,11 +953,10 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
 #pragma unroll
         for (int u = 0; u < WPT; ++u) {
             const int idx = tg + TG * u;
-            if (idx < BN * KT / 8) {
-                const int row = idx / (KT / 8), kh = idx % (KT / 8);
-                const uint32_t d[4] = {wr[u].x, wr[u].y, wr[u].z, wr[u].w};
+            if (idx < BN * WPR) {
+                const int row = idx / WPR, kh = idx % WPR;
 #pragma unroll
-                for (int h = 0; h < 8; ++h) ws[g][buf][8 * kh + h][row] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+                for (int h = 0; h < WE; ++h) ws[g][buf][WE * kh + h][row] = WV::get(wr[u], h);
             }
         }
     };
@@ -1234,6 +1266,131 @@ __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// f32w stream kernel (FP32 weights, M <= MT <= 4): streaming GEMV / skinny GEMM.
+//
+// Work split.  Rows of W come in blocks of 8; workgroup b takes blocks b, b + G,
+// b + 2G, ... and all of K for each, so the grid reads one compact window of W
+// at a time and every output is finished inside one workgroup (no atomics, no
+// cross-workgroup step).  A step covers segments 4s .. 4s+3 of the block's 8
+// rows: 32 pieces of 256 floats (1 KB each), 32 KB of W.
+//
+// Data path.  The 256 threads load a step with coalesced 16-byte loads (one
+// wave instruction reads one 1 KB piece), one step ahead into registers, and
+// move it to LDS between two barriers.  Piece c (row c / 4, segment c % 4) sits
+// at LDS floats [260c, 260c + 256): the 16-byte pad puts the pieces that the
+// chain lanes walk in step on different banks.  x for the step's segments and
+// the MT rows is staged the same way (one 1 KB piece per row and segment).
+//
+// Order.  Wave m < MT computes x row m: its lane c < 32 runs the fmaf chain of
+// piece c from +0 in ascending k; the 4 lanes of row r (a DPP quad) fold the
+// step's 4 partials into the row's running sum in ascending segment order
+// (the first partial of the row starts the sum), and the row is stored after
+// the block's last step.
+// ---------------------------------------------------------------------------
+constexpr int kF32wRows = 8;            // W rows per block
+constexpr int kF32wSegs = 4;            // segments per step
+constexpr int kF32wPad = kChunk + 4;    // LDS floats per 1 KB piece
+
+template <int MT>
+__global__ void __launch_bounds__(256) f32w_stream_kernel(F32wArgs a) {
+    constexpr int NP = kF32wRows * kF32wSegs;   // pieces per step (32)
+    __shared__ __attribute__((aligned(16))) float wsm[NP * kF32wPad];
+    __shared__ __attribute__((aligned(16))) float xsm[MT * kF32wSegs * kF32wPad];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t M = a.M, N = a.N, K = a.K;
+    const int J = a.J;
+    const int nks = (J + kF32wSegs - 1) / kF32wSegs;          // steps per block
+    const int64_t G = gridDim.x;
+    const int64_t b = a.reverse ? (int64_t)(gridDim.x - 1 - blockIdx.x) : (int64_t)blockIdx.x;
+    const int64_t nrb = (N + kF32wRows - 1) / kF32wRows;
+    const int64_t myblocks = b < nrb ? (nrb - 1 - b) / G + 1 : 0;
+    const int64_t T = myblocks * nks;
+
+    float4 wr[NP / 4];   // this thread's 16-byte pieces of the next step: segment `wave`, rows 0..7
+    float4 xr[MT];       // and of x: segment `wave`, rows 0..MT-1
+    auto load = [&](int64_t t) {
+        const int64_t rb = b + (t / nks) * G;
+        const int64_t j = (int64_t)(t % nks) * kF32wSegs + wave;
+        const int64_t len = j < J ? (K - j * kChunk < kChunk ? K - j * kChunk : kChunk) : 0;
+        const bool kin = 4 * lane < len;
+#pragma unroll
+        for (int r = 0; r < kF32wRows; ++r) {
+            const int64_t n = rb * kF32wRows + r;
+            wr[r] = (kin && n < N) ? *reinterpret_cast<const float4*>(a.w + n * K + j * kChunk + 4 * lane)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+            xr[m] = (kin && m < M) ? *reinterpret_cast<const float4*>(a.x + m * K + j * kChunk + 4 * lane)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+    };
+
+    float yrun = 0.0f;   // compute lanes: running fold of row (lane / 4) for x row `wave`
+    if (T > 0) load(0);
+    for (int64_t t = 0; t < T; ++t) {
+        __syncthreads();                                    // the previous step's chains are done
+#pragma unroll
+        for (int r = 0; r < kF32wRows; ++r)
+            *reinterpret_cast<float4*>(&wsm[(kF32wSegs * r + wave) * kF32wPad + 4 * lane]) = wr[r];
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+            *reinterpret_cast<float4*>(&xsm[(kF32wSegs * m + wave) * kF32wPad + 4 * lane]) = xr[m];
+        __syncthreads();
+        if (t + 1 < T) load(t + 1);                         // in flight during the chains
+        if (wave < MT && lane < NP) {
+            const int ks = (int)(t % nks);
+            const int c = lane, s = c % kF32wSegs;
+            const int64_t j = (int64_t)ks * kF32wSegs + s;
+            const int len = j < J ? (int)(K - j * kChunk < kChunk ? K - j * kChunk : kChunk) : 0;
+            const float* wp = &wsm[c * kF32wPad];
+            const float* xp = &xsm[(kF32wSegs * wave + s) * kF32wPad];
+            float acc = 0.0f;
+            if (len == kChunk) {
+#pragma unroll 4
+                for (int q = 0; q < kChunk / 16; ++q) {
+                    float4 wv[4], xv[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        wv[i] = *reinterpret_cast<const float4*>(wp + 16 * q + 4 * i);
+                        xv[i] = *reinterpret_cast<const float4*>(xp + 16 * q + 4 * i);
+                    }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        acc = __builtin_fmaf(xv[i].x, wv[i].x, acc);
+                        acc = __builtin_fmaf(xv[i].y, wv[i].y, acc);
+                        acc = __builtin_fmaf(xv[i].z, wv[i].z, acc);
+                        acc = __builtin_fmaf(xv[i].w, wv[i].w, acc);
+                    }
+                }
+            } else {
+                for (int q = 0; q < len; q += 4) {
+                    const float4 wv = *reinterpret_cast<const float4*>(wp + q);
+                    const float4 xv = *reinterpret_cast<const float4*>(xp + q);
+                    acc = __builtin_fmaf(xv.x, wv.x, acc);
+                    acc = __builtin_fmaf(xv.y, wv.y, acc);
+                    acc = __builtin_fmaf(xv.z, wv.z, acc);
+                    acc = __builtin_fmaf(xv.w, wv.w, acc);
+                }
+            }
+            // the 4 partials of row c / 4 (quad lanes 0..3 = segments 4ks .. 4ks+3), in order
+            const float p0 = quad_bcast<0>(acc), p1 = quad_bcast<1>(acc);
+            const float p2 = quad_bcast<2>(acc), p3 = quad_bcast<3>(acc);
+            const int nseg = J - ks * kF32wSegs;            // >= 1
+            float y = (ks == 0) ? p0 : yrun + p0;
+            if (nseg > 1) y = y + p1;
+            if (nseg > 2) y = y + p2;
+            if (nseg > 3) y = y + p3;
+            yrun = y;
+            if (ks == nks - 1 && s == 0) {
+                const int64_t n = (b + (t / nks) * G) * kF32wRows + c / kF32wSegs;
+                if (n < N && wave < M) a.y[wave * N + n] = y;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // cast kernel (comparison point only: the transient FP32 weight copy)
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) cast_kernel(const uint16_t* __restrict__ w, float* __restrict__ o,
@@ -1284,10 +1441,21 @@ __global__ void __launch_bounds__(256) argmax_kernel(const float* __restrict__ y
 // ---------------------------------------------------------------------------
 // host-side launchers
 // ---------------------------------------------------------------------------
+template <typename WT>
+static hipError_t launch_generic_t(const float* x, const WT* w, const float* bias, float* y, int64_t M, int64_t N,
+                                   int64_t K, int grid, int reverse, hipStream_t stream) {
+    hipLaunchKernelGGL(generic_kernel<WT>, dim3(grid), dim3(256), 0, stream, x, w, bias, y, M, N, K, reverse);
+    return hipGetLastError();
+}
+
 hipError_t launch_generic(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N,
                           int64_t K, int grid, int reverse, hipStream_t stream) {
-    hipLaunchKernelGGL(generic_kernel, dim3(grid), dim3(256), 0, stream, x, w, bias, y, M, N, K, reverse);
-    return hipGetLastError();
+    return launch_generic_t(x, w, bias, y, M, N, K, grid, reverse, stream);
+}
+
+hipError_t launch_generic(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N,
+                          int64_t K, int grid, int reverse, hipStream_t stream) {
+    return launch_generic_t(x, w, bias, y, M, N, K, grid, reverse, stream);
 }
 
 template <int MT, int NW, int DEPTH>
@@ -1381,28 +1549,40 @@ hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int dept
     }
 }
 
-hipError_t launch_tiled(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int reverse, hipStream_t stream) {
+template <typename WT>
+static hipError_t launch_tiled_t(const float* x, const WT* w, const float* bias, float* y, int64_t M, int64_t N,
+                                 int64_t K, int bm, int bn, int reverse, hipStream_t stream) {
     const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid((unsigned)tiles), block(256);
-    if (bm == 128 && bn == 128) hipLaunchKernelGGL((tiled_kernel<128, 128>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
-    else if (bm == 64 && bn == 128) hipLaunchKernelGGL((tiled_kernel<64, 128>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
-    else if (bm == 64 && bn == 64) hipLaunchKernelGGL((tiled_kernel<64, 64>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
+    if (bm == 128 && bn == 128) hipLaunchKernelGGL((tiled_kernel<128, 128, WT>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
+    else if (bm == 64 && bn == 128) hipLaunchKernelGGL((tiled_kernel<64, 128, WT>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
+    else if (bm == 64 && bn == 64) hipLaunchKernelGGL((tiled_kernel<64, 64, WT>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
+hipError_t launch_tiled(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int reverse, hipStream_t stream) {
+    return launch_tiled_t(x, w, bias, y, M, N, K, bm, bn, reverse, stream);
+}
+
+hipError_t launch_tiled(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int reverse, hipStream_t stream) {
+    return launch_tiled_t(x, w, bias, y, M, N, K, bm, bn, reverse, stream);
+}
+
 // Small-M tiles (16 outputs per thread, K shared out over KS = 16 * nt / (bm * bn) groups).
-hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int nt, int reverse, hipStream_t stream) {
+template <typename WT>
+static hipError_t launch_ktile_t(const float* x, const WT* w, const float* bias, float* y, int64_t M, int64_t N,
+                                 int64_t K, int bm, int bn, int nt, int reverse, hipStream_t stream) {
     const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid((unsigned)tiles);
 #define RG_KT(BM, BN, NT) \
     if (bm == BM && bn == BN && nt == NT) { \
-        hipLaunchKernelGGL((ktile_kernel<BM, BN, 16 * NT / (BM * BN), NT>), grid, dim3(NT), 0, stream, x, w, bias, y, M, N, K, \
-                           reverse); \
+        hipLaunchKernelGGL((ktile_kernel<BM, BN, 16 * NT / (BM * BN), NT, WT>), grid, dim3(NT), 0, stream, x, w, bias, y, M, \
+                           N, K, reverse); \
         return hipGetLastError(); \
     }
     RG_KT(16, 16, 256) RG_KT(16, 32, 256) RG_KT(16, 64, 256) RG_KT(32, 16, 256) RG_KT(32, 32, 256) RG_KT(32, 64, 256)
@@ -1410,6 +1590,24 @@ hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, fl
     RG_KT(16, 16, 512) RG_KT(32, 16, 512) RG_KT(64, 16, 512)
 #undef RG_KT
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int nt, int reverse, hipStream_t stream) {
+    return launch_ktile_t(x, w, bias, y, M, N, K, bm, bn, nt, reverse, stream);
+}
+
+hipError_t launch_ktile(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                        int bm, int bn, int nt, int reverse, hipStream_t stream) {
+    return launch_ktile_t(x, w, bias, y, M, N, K, bm, bn, nt, reverse, stream);
+}
+
+hipError_t launch_f32w_stream(const F32wArgs& a, int mt, int grid, hipStream_t stream) {
+    if (mt == 1) hipLaunchKernelGGL(f32w_stream_kernel<1>, dim3(grid), dim3(256), 0, stream, a);
+    else if (mt == 2) hipLaunchKernelGGL(f32w_stream_kernel<2>, dim3(grid), dim3(256), 0, stream, a);
+    else if (mt == 4) hipLaunchKernelGGL(f32w_stream_kernel<4>, dim3(grid), dim3(256), 0, stream, a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
 }
 
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream) {

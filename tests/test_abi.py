@@ -172,3 +172,32 @@ def test_negative_control_library_exports_its_header_and_checks_arguments():
     assert L.rg_negctl_atomic_splitk(0x1002, 0x2000, 0x3000, 1, 1, 8, 2, None) == negctl.RG_NEGCTL_ERR_INVAL
     assert L.rg_negctl_cu_split(0x1000, 0x2000, 0x3000, 0, 1, 8, None, None) == negctl.RG_NEGCTL_ERR_INVAL
     assert L.rg_negctl_cu_split(0x1000, 0x2001, 0x3000, 1, 1, 8, None, None) == negctl.RG_NEGCTL_ERR_INVAL
+
+
+def test_f32w_planner_and_argument_checks():
+    rg.rg_linear_set_launch(None)
+    assert rg.rg_plan_f32w(1, 4096, 14336)["kernel_name"] == "f32w_stream"
+    assert rg.rg_plan_f32w(4, 6144, 4096)["kernel_name"] == "f32w_stream"
+    assert rg.rg_plan_f32w(16, 6144, 4096)["kernel_name"] == "ktile"
+    assert rg.rg_plan_f32w(100, 1000, 1000)["kernel_name"] == "tiled"
+    assert rg.rg_plan_f32w(1, 100, 1001)["kernel_name"] == "generic"      # K % 4 != 0
+    assert rg.rg_plan_f32w(1, 4096, 4100)["nchunks"] == 17
+    try:
+        for k in ("decode", "decode_xs", "gemv"):
+            rg.rg_linear_set_launch(kernel=k)
+            with pytest.raises(rg.RgError):
+                rg.rg_plan_f32w(1, 4096, 4096)
+        rg.rg_linear_set_launch(kernel="f32w_stream")
+        with pytest.raises(rg.RgError):
+            rg.rg_plan(1, 4096, 4096)               # the BF16 path has no such kernel
+        with pytest.raises(rg.RgError):
+            rg.rg_plan_f32w(5, 4096, 4096)          # M <= 4 only
+        rg.rg_linear_set_launch(kernel="ktile")
+        assert rg.rg_plan_f32w(1, 4096, 4096)["kernel_name"] == "ktile"
+    finally:
+        rg.rg_linear_set_launch(None)
+    L = rg.lib
+    assert L.rg_linear_f32w(None, 0x1000, 0x2000, 1, 1, 1, None) == rg.RG_ERR_INVAL
+    assert L.rg_linear_f32w(0x1000, 0x2002, 0x3000, 1, 1, 1, None) == rg.RG_ERR_ALIGN
+    assert L.rg_linear_f32w(0x1000, 0x2000, 0x1000, 1, 1, 1, None) == rg.RG_ERR_ALIAS
+    assert L.rg_linear_f32w(0x1000, 0x2000, 0x3000, 1, 0, 1, None) == rg.RG_ERR_INVAL
