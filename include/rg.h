@@ -72,8 +72,8 @@ typedef enum {
     RG_KERNEL_TILED = 2,     /* larger M: register-tiled kernel, whole K per workgroup */
     RG_KERNEL_DECODE_XS = 3, /* M == 1: streaming GEMV with x streamed through LDS beside W */
     RG_KERNEL_GEMV = 4,      /* M == 1, K % 256 == 0, K >= 4096: 32 KB W bursts, whole rows per wave */
-    RG_KERNEL_F32W_STREAM = 5, /* FP32 weights only (rg_linear_f32w), M <= 4: 8-row blocks streamed
-                                  through LDS, one chain per lane */
+    RG_KERNEL_STREAM = 5,    /* M <= 4: 8-row blocks of W streamed through LDS, one chain per lane
+                                (FP32 weights by default; BF16 weights when forced) */
     RG_KERNEL_KTILE = 6      /* 4 < M <= 64 (any M when forced): 4 x 4 register tiles, K segments
                                 shared out over thread groups */
 } rg_kernel_id;
@@ -150,7 +150,7 @@ int rg_linear_bias(const float* x, const uint16_t* w_bf16, const float* bias, fl
  *   x      device pointer, float32 [M][K], 4-byte aligned
  *   w_f32  device pointer, float32 [N][K], 4-byte aligned
  *   y      device pointer, float32 [M][N], 4-byte aligned, must not overlap x or W
- * Kernels: RG_KERNEL_F32W_STREAM for M <= 4, then ktile (M <= 64) and tiled,
+ * Kernels: RG_KERNEL_STREAM for M <= 4, then ktile (M <= 64) and tiled,
  * all needing 16-byte aligned x and W and K % 4 == 0; other shapes take the
  * generic kernel.  Errors, streams and ownership as rg_linear; the same
  * rg_linear_set_launch overrides apply (decode, decode_xs and gemv cannot be

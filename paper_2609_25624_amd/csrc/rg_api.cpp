@@ -213,6 +213,34 @@ bool ktile_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan*
     return true;
 }
 
+hipError_t launch_stream(const float* x, const void* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
+                         const Plan& p, bool f32_weights, hipStream_t st) {
+    rg::StreamArgs a;
+    a.x = x;
+    a.w = w;
+    a.bias = bias;
+    a.y = y;
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    a.J = (int)ceil_div(K, rg::kChunk);
+    a.reverse = p.reverse;
+    return rg::launch_stream(a, f32_weights, p.mt, p.grid, st);
+}
+
+// 8-row blocks of W, up to 8 workgroups per CU (measured: more workgroups in
+// flight stream the large layers faster).
+bool stream_schedule(int64_t M, int64_t N, const rg_launch_t& o, Plan* p) {
+    if ((o.waves_per_wg > 0 && o.waves_per_wg != 4) || o.depth > 0 || o.tile_n > 0) return false;
+    const int64_t blocks = ceil_div(N, 8);
+    const int64_t grid = o.grid_wgs > 0 ? o.grid_wgs : (blocks < 8 * kNominalCUs ? blocks : 8 * kNominalCUs);
+    p->mt = M <= 1 ? 1 : (M <= 2 ? 2 : 4);
+    p->grid = (int)grid;
+    p->nw = 4;
+    p->rq = 2;                                    // reported as 8 rows per round
+    return true;
+}
+
 // Register-tiled kernel: the largest tile that still gives every CU a few workgroups.
 int tiled_schedule(int64_t M, int64_t N, Plan* p) {
     const int64_t t128 = ceil_div(M, 128) * ceil_div(N, 128);
@@ -265,7 +293,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         if (want == RG_KERNEL_TILED && !tiled_ok) return RG_ERR_RANGE;
         if (want == RG_KERNEL_GEMV && !gemv_ok) return RG_ERR_RANGE;
         if (want == RG_KERNEL_KTILE && !fast_ok) return RG_ERR_RANGE;   // any M when forced
-        if (want == RG_KERNEL_F32W_STREAM) return RG_ERR_RANGE;   // FP32 weights only
+        if (want == RG_KERNEL_STREAM && !(fast_ok && M <= 4)) return RG_ERR_RANGE;
     }
     p->mslices = 1;
     p->kernel = want;
@@ -274,6 +302,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         if (ktile_schedule(M, N, K, o, p)) return RG_OK;
         return RG_ERR_RANGE;
     }
+    if (want == RG_KERNEL_STREAM) return stream_schedule(M, N, o, p) ? RG_OK : RG_ERR_RANGE;
     if (want == RG_KERNEL_GEMV) {
         if (gemv_schedule(N, K, o, p)) return RG_OK;
         if (forced) return RG_ERR_RANGE;
@@ -309,7 +338,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
 // templated on the element type).
 int make_plan_f32w(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& o, Plan* p) {
     int want = RG_KERNEL_GENERIC;
-    if (fast_ok && M <= 4) want = RG_KERNEL_F32W_STREAM;
+    if (fast_ok && M <= 4) want = RG_KERNEL_STREAM;
     else if (fast_ok && M <= kDecodeMaxM) want = RG_KERNEL_KTILE;
     else if (fast_ok) want = RG_KERNEL_TILED;
     const bool forced = o.kernel > 0;
@@ -317,23 +346,12 @@ int make_plan_f32w(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launc
         want = o.kernel - 1;
         if (want == RG_KERNEL_DECODE || want == RG_KERNEL_DECODE_XS || want == RG_KERNEL_GEMV) return RG_ERR_RANGE;
         if (want != RG_KERNEL_GENERIC && !fast_ok) return RG_ERR_RANGE;
-        if (want == RG_KERNEL_F32W_STREAM && M > 4) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_STREAM && M > 4) return RG_ERR_RANGE;
     }
     p->kernel = want;
     p->reverse = o.grid_order;
     p->mslices = 1;
-    if (want == RG_KERNEL_F32W_STREAM) {
-        if ((o.waves_per_wg > 0 && o.waves_per_wg != 4) || o.depth > 0 || o.tile_n > 0) return RG_ERR_RANGE;
-        // 8-row blocks of W; up to 8 workgroups per CU (measured: more workgroups in flight
-        // stream the large layers faster)
-        const int64_t blocks = ceil_div(N, 8);
-        int64_t grid = o.grid_wgs > 0 ? o.grid_wgs : (blocks < 8 * kNominalCUs ? blocks : 8 * kNominalCUs);
-        p->mt = M <= 1 ? 1 : (M <= 2 ? 2 : 4);
-        p->grid = (int)grid;
-        p->nw = 4;
-        p->rq = 2;                                    // reported as 8 rows per round
-        return RG_OK;
-    }
+    if (want == RG_KERNEL_STREAM) return stream_schedule(M, N, o, p) ? RG_OK : RG_ERR_RANGE;
     if (want == RG_KERNEL_KTILE) return ktile_schedule(M, N, K, o, p) ? RG_OK : RG_ERR_RANGE;
     if (want == RG_KERNEL_TILED) return tiled_schedule(M, N, p);
     generic_schedule(M, N, o, p);
@@ -499,6 +517,8 @@ int linear_impl(const float* x, const uint16_t* w, const float* bias, float* y, 
         if (!p.x_streamed && blocks > 0x7fffffff) return RG_ERR_RANGE;
         e = p.x_streamed ? rg::launch_decode1(a, p.grid, p.nw, p.depth, st)
                          : rg::launch_decode(a, p.mt, (int)blocks, p.nw, p.depth, st);
+    } else if (p.kernel == RG_KERNEL_STREAM) {
+        e = launch_stream(x, w, bias, y, M, N, K, p, false, st);
     } else if (p.kernel == RG_KERNEL_KTILE) {
         e = rg::launch_ktile(x, w, bias, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.reverse, st);
     } else if (p.kernel == RG_KERNEL_TILED) {
@@ -525,17 +545,8 @@ int linear_f32w_impl(const float* x, const float* w, float* y, int64_t M, int64_
     hipStream_t st = (hipStream_t)stream;
     (void)hipGetLastError();
     hipError_t e = hipSuccess;
-    if (p.kernel == RG_KERNEL_F32W_STREAM) {
-        rg::F32wArgs a;
-        a.x = x;
-        a.w = w;
-        a.y = y;
-        a.M = M;
-        a.N = N;
-        a.K = K;
-        a.J = (int)ceil_div(K, rg::kChunk);
-        a.reverse = p.reverse;
-        e = rg::launch_f32w_stream(a, p.mt, p.grid, st);
+    if (p.kernel == RG_KERNEL_STREAM) {
+        e = launch_stream(x, w, nullptr, y, M, N, K, p, true, st);
     } else if (p.kernel == RG_KERNEL_KTILE) {
         e = rg::launch_ktile(x, w, nullptr, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.reverse, st);
     } else if (p.kernel == RG_KERNEL_TILED) {

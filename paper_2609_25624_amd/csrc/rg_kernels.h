@@ -39,21 +39,23 @@ struct GemvArgs {
     int reverse;        // 1: workgroup b takes the quads of workgroup grid-1-b
 };
 
-// FP32-weight streaming kernel (M <= mt <= 4, K % 4 == 0, x and w 16-byte aligned).
-struct F32wArgs {
+// Streaming kernel through LDS (M <= mt <= 4; K % 8 == 0 for BF16 or K % 4 == 0
+// for FP32 weights; x and w 16-byte aligned).
+struct StreamArgs {
     const float* x;
-    const float* w;
+    const void* w;        // uint16_t bfloat16 bits or float, [N][K]
+    const float* bias;    // b[N] added after the fold, or null
     float* y;
     int64_t M, N, K;
-    int J;          // ceil(K / kChunk)
-    int reverse;    // reversed workgroup-to-block mapping
+    int J;                // ceil(K / kChunk)
+    int reverse;          // reversed workgroup-to-block mapping
 };
 
 hipError_t launch_generic(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N,
                           int64_t K, int grid, int reverse, hipStream_t stream);
 hipError_t launch_generic(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N,
                           int64_t K, int grid, int reverse, hipStream_t stream);
-hipError_t launch_f32w_stream(const F32wArgs& a, int mt, int grid, hipStream_t stream);
+hipError_t launch_stream(const StreamArgs& a, bool f32_weights, int mt, int grid, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_gemv(const GemvArgs& a, int grid, int nw, hipStream_t stream);

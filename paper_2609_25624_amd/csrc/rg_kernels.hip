@@ -1266,126 +1266,139 @@ __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// f32w stream kernel (FP32 weights, M <= MT <= 4): streaming GEMV / skinny GEMM.
+// stream kernel (M <= MT <= 4; FP32 or BF16 weights): streaming GEMV / skinny GEMM.
 //
 // Work split.  Rows of W come in blocks of 8; workgroup b takes blocks b, b + G,
 // b + 2G, ... and all of K for each, so the grid reads one compact window of W
 // at a time and every output is finished inside one workgroup (no atomics, no
-// cross-workgroup step).  A step covers segments 4s .. 4s+3 of the block's 8
-// rows: 32 pieces of 256 floats (1 KB each), 32 KB of W.
+// cross-workgroup step).  A step covers the next 4 KB of each of the block's 8
+// rows: SEGS = 4 (FP32) or 8 (BF16) segments of 256 weights, 32 KB of W.
 //
 // Data path.  The 256 threads load a step with coalesced 16-byte loads (one
-// wave instruction reads one 1 KB piece), one step ahead into registers, and
-// move it to LDS between two barriers.  Piece c (row c / 4, segment c % 4) sits
-// at LDS floats [260c, 260c + 256): the 16-byte pad puts the pieces that the
-// chain lanes walk in step on different banks.  x for the step's segments and
-// the MT rows is staged the same way (one 1 KB piece per row and segment).
+// wave instruction reads 1 KB of one row), one step ahead into registers, and
+// move it to LDS between two barriers.  Piece c (row c / SEGS, segment
+// c % SEGS) sits in LDS at a stride of 256 weights + 16 bytes, so the lanes
+// that walk the pieces in step read different banks.  x for the step's segments
+// and the MT rows is staged the same way (one 1 KB piece per row and segment).
 //
-// Order.  Wave m < MT computes x row m: its lane c < 32 runs the fmaf chain of
-// piece c from +0 in ascending k; the 4 lanes of row r (a DPP quad) fold the
-// step's 4 partials into the row's running sum in ascending segment order
-// (the first partial of the row starts the sum), and the row is stored after
-// the block's last step.
+// Order.  Wave m < MT computes x row m: its lane c < 8 * SEGS runs the fmaf
+// chain of piece c from +0 in ascending k; the SEGS lanes of a row fold the
+// step's partials into the row's running sum in ascending segment order (the
+// first partial of the row starts the sum), and the row is stored, plus b[n]
+// for the bias variant, after the block's last step.
 // ---------------------------------------------------------------------------
-constexpr int kF32wRows = 8;            // W rows per block
-constexpr int kF32wSegs = 4;            // segments per step
-constexpr int kF32wPad = kChunk + 4;    // LDS floats per 1 KB piece
+constexpr int kStreamRows = 8;          // W rows per block
 
-template <int MT>
-__global__ void __launch_bounds__(256) f32w_stream_kernel(F32wArgs a) {
-    constexpr int NP = kF32wRows * kF32wSegs;   // pieces per step (32)
-    __shared__ __attribute__((aligned(16))) float wsm[NP * kF32wPad];
-    __shared__ __attribute__((aligned(16))) float xsm[MT * kF32wSegs * kF32wPad];
+template <int MT, typename WT>
+__global__ void __launch_bounds__(256) stream_kernel(StreamArgs a) {
+    using WV = WVec<WT>;
+    constexpr int EPV = WV::E;                          // weights per 16-byte vector
+    constexpr int SEGS = 4096 / (kChunk * (int)sizeof(WT));   // segments per 4 KB row step
+    constexpr int NP = kStreamRows * SEGS;              // pieces (chains) per step: 32 or 64
+    constexpr int WPAD = kChunk + 16 / (int)sizeof(WT); // LDS weights per piece
+    constexpr int XPAD = kChunk + 4;                    // LDS floats per x piece
+    constexpr int XV = SEGS * 64 / 256;                 // x float4 loads per thread per row
+    static_assert(NP <= 64, "one chain per lane");
+    __shared__ __attribute__((aligned(16))) WT wsm[NP * WPAD];
+    __shared__ __attribute__((aligned(16))) float xsm[MT * SEGS * XPAD];
 
+    const WT* __restrict__ w = reinterpret_cast<const WT*>(a.w);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t M = a.M, N = a.N, K = a.K;
     const int J = a.J;
-    const int nks = (J + kF32wSegs - 1) / kF32wSegs;          // steps per block
+    const int nks = (J + SEGS - 1) / SEGS;              // steps per block
     const int64_t G = gridDim.x;
     const int64_t b = a.reverse ? (int64_t)(gridDim.x - 1 - blockIdx.x) : (int64_t)blockIdx.x;
-    const int64_t nrb = (N + kF32wRows - 1) / kF32wRows;
+    const int64_t nrb = (N + kStreamRows - 1) / kStreamRows;
     const int64_t myblocks = b < nrb ? (nrb - 1 - b) / G + 1 : 0;
     const int64_t T = myblocks * nks;
 
-    float4 wr[NP / 4];   // this thread's 16-byte pieces of the next step: segment `wave`, rows 0..7
-    float4 xr[MT];       // and of x: segment `wave`, rows 0..MT-1
+    // this thread's W vector of each row: element e0 of the row's 4 KB step window
+    const int e0 = wave * (1024 / (int)sizeof(WT)) + lane * EPV;
+    const int wl = (e0 / kChunk) * WPAD + e0 % kChunk;  // its LDS offset inside the row's pieces
+    typename WV::V wr[kStreamRows];
+    float4 xr[MT][XV];
     auto load = [&](int64_t t) {
         const int64_t rb = b + (t / nks) * G;
-        const int64_t j = (int64_t)(t % nks) * kF32wSegs + wave;
-        const int64_t len = j < J ? (K - j * kChunk < kChunk ? K - j * kChunk : kChunk) : 0;
-        const bool kin = 4 * lane < len;
+        const int64_t k0 = (int64_t)(t % nks) * SEGS * kChunk;
 #pragma unroll
-        for (int r = 0; r < kF32wRows; ++r) {
-            const int64_t n = rb * kF32wRows + r;
-            wr[r] = (kin && n < N) ? *reinterpret_cast<const float4*>(a.w + n * K + j * kChunk + 4 * lane)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int r = 0; r < kStreamRows; ++r) {
+            const int64_t n = rb * kStreamRows + r;
+            wr[r] = (n < N && k0 + e0 < K) ? *reinterpret_cast<const typename WV::V*>(w + n * K + k0 + e0)
+                                           : WV::zero();
         }
 #pragma unroll
         for (int m = 0; m < MT; ++m)
-            xr[m] = (kin && m < M) ? *reinterpret_cast<const float4*>(a.x + m * K + j * kChunk + 4 * lane)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int u = 0; u < XV; ++u) {
+                const int64_t k = k0 + 4 * (tid + 256 * u);
+                xr[m][u] = (m < M && k < K) ? *reinterpret_cast<const float4*>(a.x + m * K + k)
+                                            : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
     };
 
-    float yrun = 0.0f;   // compute lanes: running fold of row (lane / 4) for x row `wave`
+    float yrun = 0.0f;   // compute lanes: running fold of row (lane / SEGS) for x row `wave`
+    float bval = 0.0f;
     if (T > 0) load(0);
     for (int64_t t = 0; t < T; ++t) {
         __syncthreads();                                    // the previous step's chains are done
 #pragma unroll
-        for (int r = 0; r < kF32wRows; ++r)
-            *reinterpret_cast<float4*>(&wsm[(kF32wSegs * r + wave) * kF32wPad + 4 * lane]) = wr[r];
+        for (int r = 0; r < kStreamRows; ++r)
+            *reinterpret_cast<typename WV::V*>(&wsm[r * SEGS * WPAD + wl]) = wr[r];
 #pragma unroll
         for (int m = 0; m < MT; ++m)
-            *reinterpret_cast<float4*>(&xsm[(kF32wSegs * m + wave) * kF32wPad + 4 * lane]) = xr[m];
+#pragma unroll
+            for (int u = 0; u < XV; ++u) {
+                const int q = tid + 256 * u;                // float4 q of the x window: segment q / 64
+                *reinterpret_cast<float4*>(&xsm[(SEGS * m + q / 64) * XPAD + 4 * (q % 64)]) = xr[m][u];
+            }
         __syncthreads();
+        const int ks = (int)(t % nks);
+        const int c = lane, s = c % SEGS;
+        const bool computes = wave < MT && c < NP;
+        const bool stores = computes && ks == nks - 1 && s == 0;
+        const int64_t n = (b + (t / nks) * G) * kStreamRows + c / SEGS;
+        if (stores && a.bias && n < N) bval = a.bias[n];   // issued before the next step's loads
         if (t + 1 < T) load(t + 1);                         // in flight during the chains
-        if (wave < MT && lane < NP) {
-            const int ks = (int)(t % nks);
-            const int c = lane, s = c % kF32wSegs;
-            const int64_t j = (int64_t)ks * kF32wSegs + s;
+        if (computes) {
+            const int64_t j = (int64_t)ks * SEGS + s;
             const int len = j < J ? (int)(K - j * kChunk < kChunk ? K - j * kChunk : kChunk) : 0;
-            const float* wp = &wsm[c * kF32wPad];
-            const float* xp = &xsm[(kF32wSegs * wave + s) * kF32wPad];
+            const WT* wp = &wsm[c * WPAD];
+            const float* xp = &xsm[(SEGS * wave + s) * XPAD];
             float acc = 0.0f;
+            auto piece = [&](int e) {                       // EPV weights at element e of the piece
+                const typename WV::V wv = *reinterpret_cast<const typename WV::V*>(wp + e);
+                float xv[EPV];
+#pragma unroll
+                for (int i = 0; i < EPV; i += 4) {
+                    const float4 x4 = *reinterpret_cast<const float4*>(xp + e + i);
+                    xv[i] = x4.x; xv[i + 1] = x4.y; xv[i + 2] = x4.z; xv[i + 3] = x4.w;
+                }
+#pragma unroll
+                for (int i = 0; i < EPV; ++i) acc = __builtin_fmaf(xv[i], WV::get(wv, i), acc);
+            };
             if (len == kChunk) {
-#pragma unroll 4
-                for (int q = 0; q < kChunk / 16; ++q) {
-                    float4 wv[4], xv[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        wv[i] = *reinterpret_cast<const float4*>(wp + 16 * q + 4 * i);
-                        xv[i] = *reinterpret_cast<const float4*>(xp + 16 * q + 4 * i);
-                    }
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        acc = __builtin_fmaf(xv[i].x, wv[i].x, acc);
-                        acc = __builtin_fmaf(xv[i].y, wv[i].y, acc);
-                        acc = __builtin_fmaf(xv[i].z, wv[i].z, acc);
-                        acc = __builtin_fmaf(xv[i].w, wv[i].w, acc);
-                    }
-                }
+#pragma unroll 8
+                for (int e = 0; e < kChunk; e += EPV) piece(e);
             } else {
-                for (int q = 0; q < len; q += 4) {
-                    const float4 wv = *reinterpret_cast<const float4*>(wp + q);
-                    const float4 xv = *reinterpret_cast<const float4*>(xp + q);
-                    acc = __builtin_fmaf(xv.x, wv.x, acc);
-                    acc = __builtin_fmaf(xv.y, wv.y, acc);
-                    acc = __builtin_fmaf(xv.z, wv.z, acc);
-                    acc = __builtin_fmaf(xv.w, wv.w, acc);
-                }
+                for (int e = 0; e < len; e += EPV) piece(e);
             }
-            // the 4 partials of row c / 4 (quad lanes 0..3 = segments 4ks .. 4ks+3), in order
-            const float p0 = quad_bcast<0>(acc), p1 = quad_bcast<1>(acc);
-            const float p2 = quad_bcast<2>(acc), p3 = quad_bcast<3>(acc);
-            const int nseg = J - ks * kF32wSegs;            // >= 1
-            float y = (ks == 0) ? p0 : yrun + p0;
-            if (nseg > 1) y = y + p1;
-            if (nseg > 2) y = y + p2;
-            if (nseg > 3) y = y + p3;
+            // the row's SEGS partials (lanes SEGS*r .. SEGS*r + SEGS-1), folded in order
+            float p[SEGS];
+            if constexpr (SEGS == 4) {
+                p[0] = quad_bcast<0>(acc); p[1] = quad_bcast<1>(acc);
+                p[2] = quad_bcast<2>(acc); p[3] = quad_bcast<3>(acc);
+            } else {
+#pragma unroll
+                for (int i = 0; i < SEGS; ++i) p[i] = __shfl(acc, (c & ~(SEGS - 1)) + i, 64);
+            }
+            const int nseg = J - ks * SEGS;                 // >= 1
+            float y = (ks == 0) ? p[0] : yrun + p[0];
+#pragma unroll
+            for (int i = 1; i < SEGS; ++i)
+                if (i < nseg) y = y + p[i];
             yrun = y;
-            if (ks == nks - 1 && s == 0) {
-                const int64_t n = (b + (t / nks) * G) * kF32wRows + c / kF32wSegs;
-                if (n < N && wave < M) a.y[wave * N + n] = y;
-            }
+            if (stores && n < N && wave < M) a.y[wave * N + n] = a.bias ? y + bval : y;
         }
     }
 }
@@ -1602,12 +1615,17 @@ hipError_t launch_ktile(const float* x, const float* w, const float* bias, float
     return launch_ktile_t(x, w, bias, y, M, N, K, bm, bn, nt, reverse, stream);
 }
 
-hipError_t launch_f32w_stream(const F32wArgs& a, int mt, int grid, hipStream_t stream) {
-    if (mt == 1) hipLaunchKernelGGL(f32w_stream_kernel<1>, dim3(grid), dim3(256), 0, stream, a);
-    else if (mt == 2) hipLaunchKernelGGL(f32w_stream_kernel<2>, dim3(grid), dim3(256), 0, stream, a);
-    else if (mt == 4) hipLaunchKernelGGL(f32w_stream_kernel<4>, dim3(grid), dim3(256), 0, stream, a);
+template <typename WT>
+static hipError_t launch_stream_t(const StreamArgs& a, int mt, int grid, hipStream_t stream) {
+    if (mt == 1) hipLaunchKernelGGL((stream_kernel<1, WT>), dim3(grid), dim3(256), 0, stream, a);
+    else if (mt == 2) hipLaunchKernelGGL((stream_kernel<2, WT>), dim3(grid), dim3(256), 0, stream, a);
+    else if (mt == 4) hipLaunchKernelGGL((stream_kernel<4, WT>), dim3(grid), dim3(256), 0, stream, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
+}
+
+hipError_t launch_stream(const StreamArgs& a, bool f32_weights, int mt, int grid, hipStream_t stream) {
+    return f32_weights ? launch_stream_t<float>(a, mt, grid, stream) : launch_stream_t<uint16_t>(a, mt, grid, stream);
 }
 
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream) {

@@ -176,8 +176,8 @@ def test_negative_control_library_exports_its_header_and_checks_arguments():
 
 def test_f32w_planner_and_argument_checks():
     rg.rg_linear_set_launch(None)
-    assert rg.rg_plan_f32w(1, 4096, 14336)["kernel_name"] == "f32w_stream"
-    assert rg.rg_plan_f32w(4, 6144, 4096)["kernel_name"] == "f32w_stream"
+    assert rg.rg_plan_f32w(1, 4096, 14336)["kernel_name"] == "stream"
+    assert rg.rg_plan_f32w(4, 6144, 4096)["kernel_name"] == "stream"
     assert rg.rg_plan_f32w(16, 6144, 4096)["kernel_name"] == "ktile"
     assert rg.rg_plan_f32w(100, 1000, 1000)["kernel_name"] == "tiled"
     assert rg.rg_plan_f32w(1, 100, 1001)["kernel_name"] == "generic"      # K % 4 != 0
@@ -187,9 +187,10 @@ def test_f32w_planner_and_argument_checks():
             rg.rg_linear_set_launch(kernel=k)
             with pytest.raises(rg.RgError):
                 rg.rg_plan_f32w(1, 4096, 4096)
-        rg.rg_linear_set_launch(kernel="f32w_stream")
+        rg.rg_linear_set_launch(kernel="stream")
+        assert rg.rg_plan(4, 4096, 4096)["kernel_name"] == "stream"   # BF16 weights when forced
         with pytest.raises(rg.RgError):
-            rg.rg_plan(1, 4096, 4096)               # the BF16 path has no such kernel
+            rg.rg_plan(1, 4096, 4100)               # BF16: K % 8 == 0 only
         with pytest.raises(rg.RgError):
             rg.rg_plan_f32w(5, 4096, 4096)          # M <= 4 only
         rg.rg_linear_set_launch(kernel="ktile")

@@ -46,6 +46,7 @@ _SETTINGS = [
     dict(kernel="ktile", tile_n=64),
     dict(kernel="ktile", tile_n=16, waves_per_wg=8),
     dict(kernel="tiled"),
+    dict(kernel="stream"),
 ]
 
 

@@ -58,7 +58,7 @@ def _check(M, N, K, seed=0, kernel=None, **launch):
 @pytest.mark.parametrize("N,K", [(1, 4), (7, 252), (8, 256), (9, 260), (1030, 1000), (515, 4096), (64, 4100),
                                  (33, 14336)])
 def test_stream_kernel_shapes(M, N, K):
-    _check(M, N, K, seed=M + N + K, kernel="f32w_stream")
+    _check(M, N, K, seed=M + N + K, kernel="stream")
 
 
 @pytest.mark.parametrize("M,N,K", [(5, 300, 1000), (16, 1030, 4096), (33, 257, 2052), (64, 100, 520)])
@@ -79,7 +79,7 @@ def test_generic_with_fp32_weights(M, N, K):
 @pytest.mark.parametrize("launch", [dict(grid_wgs=1), dict(grid_wgs=7, grid_order=1), dict(grid_wgs=3000),
                                     dict(grid_order=1)])
 def test_stream_kernel_launch_settings(launch):
-    _check(2, 1030, 4352, seed=9, kernel="f32w_stream", **launch)
+    _check(2, 1030, 4352, seed=9, kernel="stream", **launch)
 
 
 def test_fp32_weight_probes_on_gpu():

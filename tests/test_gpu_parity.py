@@ -212,7 +212,19 @@ def test_ktile_shapes(M, N, K, tile_n, waves):
         rg.rg_linear_set_launch(None)
 
 
-@pytest.mark.parametrize("K,kernel", [(4352, "gemv"), (4096, "gemv"), (4096, "decode_xs")])
+@pytest.mark.parametrize("M", [1, 2, 3, 4])
+@pytest.mark.parametrize("N,K", [(1, 8), (9, 264), (1030, 4096), (33, 14336), (7, 4352), (515, 2056)])
+def test_stream_kernel_bf16_shapes(M, N, K):
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(kernel="stream")
+    try:
+        assert rg.rg_plan(M, N, K)["kernel_name"] == "stream"
+        _check_layer(M, N, K, seed=M * 7 + N + K)
+    finally:
+        rg.rg_linear_set_launch(None)
+
+
+@pytest.mark.parametrize("K,kernel", [(4352, "gemv"), (4096, "gemv"), (4096, "decode_xs"), (4096, "stream")])
 def test_order_probes_inside_m1_rows(K, kernel):
     """The hand-derived probes embedded in long rows (zero x and weight 1.0 around them) of an
     otherwise random 1030-row layer, run by the M = 1 streaming kernels and compared bitwise
@@ -312,6 +324,8 @@ def _launch_settings():
         dict(kernel="ktile", tile_n=32),
         dict(kernel="ktile", tile_n=64, grid_order=1),
         dict(kernel="ktile", tile_n=16, waves_per_wg=8),
+        dict(kernel="stream"),
+        dict(kernel="stream", grid_wgs=7, grid_order=1),
     ]
 
 
