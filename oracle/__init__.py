@@ -38,6 +38,12 @@ def lib():
         L.rg_oracle_linear_sampled.restype = ci
         L.rg_ref_fp64.argtypes = [vp, vp, vp, vp, i64, i64, i64, ci]
         L.rg_ref_fp64.restype = ci
+        L.rg_exp1.argtypes = [ctypes.c_float]
+        L.rg_exp1.restype = ctypes.c_float
+        L.rg_exp1_array.argtypes = [vp, vp, i64]
+        L.rg_exp1_array.restype = None
+        L.rg_attn_oracle.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, ctypes.c_float, vp, ci]
+        L.rg_attn_oracle.restype = ci
         L.rg_oracle_argmax.argtypes = [vp, i64]
         L.rg_oracle_argmax.restype = i64
         _lib = L
@@ -154,3 +160,33 @@ def gamma(K: int) -> float:
 def argmax(v) -> int:
     v = np.ascontiguousarray(v, dtype=np.float32).ravel()
     return int(lib().rg_oracle_argmax(v.ctypes.data, v.size))
+
+
+def exp1(u) -> np.ndarray:
+    """EXP1 (the exponential of the fixed-order attention) elementwise on float32 input."""
+    u = np.ascontiguousarray(u, dtype=np.float32)
+    out = np.empty_like(u)
+    lib().rg_exp1_array(u.ctypes.data, out.ctypes.data, u.size)
+    return out
+
+
+def attn_decode(q, kc, vc, lens, scale, nthreads=None) -> np.ndarray:
+    """Fixed-order decode attention: q f32 [B,H,D], kc/vc bf16 bits [B,Hkv,Lmax,D], lens int32 [B]."""
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    kc = np.ascontiguousarray(kc)
+    vc = np.ascontiguousarray(vc)
+    if kc.dtype != np.uint16 or vc.dtype != np.uint16:
+        raise TypeError("kc and vc must hold bfloat16 bit patterns as uint16")
+    lens = np.ascontiguousarray(lens, dtype=np.int32)
+    B, H, D = q.shape
+    _, Hkv, Lmax, D2 = kc.shape
+    if kc.shape != vc.shape or kc.shape[0] != B or D2 != D or lens.shape != (B,):
+        raise ValueError("shape mismatch")
+    nt = _threads(nthreads)
+    scratch = np.empty((nt, Lmax), dtype=np.float32)
+    out = np.empty((B, H, D), dtype=np.float32)
+    rc = lib().rg_attn_oracle(q.ctypes.data, kc.ctypes.data, vc.ctypes.data, lens.ctypes.data, out.ctypes.data,
+                              B, H, Hkv, Lmax, D, float(np.float32(scale)), scratch.ctypes.data, nt)
+    if rc != 0:
+        raise ValueError("rg_attn_oracle rejected its arguments")
+    return out

@@ -13,9 +13,12 @@ FLAGS = ["-O2", "-std=c99", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
          "-fno-unsafe-math-optimizations"]
 
 
+SOURCES = ["rg_oracle.c", "rg_attn_oracle.c"]
+
+
 def build(verbose: bool = False) -> str:
-    src = os.path.join(HERE, "rg_oracle.c")
-    cmd = ["gcc", *FLAGS, src, "-o", LIB + ".tmp", "-lm"]
+    srcs = [os.path.join(HERE, f) for f in SOURCES]
+    cmd = ["gcc", *FLAGS, *srcs, "-o", LIB + ".tmp", "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
