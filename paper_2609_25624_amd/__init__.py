@@ -61,6 +61,7 @@ def _load():
         "rg_stream_create_cu_mask": [ctypes.POINTER(ctypes.c_uint32), ctypes.c_uint32, ctypes.POINTER(vp)],
         "rg_stream_destroy": [vp],
         "rg_device_cu_count": [ctypes.POINTER(i32)],
+        "rg_attn_decode": [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, ctypes.c_float, vp, i64, vp],
         "rg_strerror": [ctypes.c_int],
         "rg_last_hip_error": [],
     }
@@ -69,6 +70,8 @@ def _load():
         f.argtypes = args
         f.restype = ctypes.c_int
     L.rg_strerror.restype = ctypes.c_char_p
+    L.rg_attn_workspace_size.argtypes = [i64, i64, i64, i64]
+    L.rg_attn_workspace_size.restype = i64
     return L
 
 
@@ -79,6 +82,8 @@ EXPORTS = ("rg_linear", "rg_linear_bias", "rg_linear_f32w", "rg_linear_set_launc
            "rg_cast_bf16_f32", "rg_argmax_rows",
            "rg_stream_create_cu_mask", "rg_stream_destroy", "rg_device_cu_count", "rg_strerror",
            "rg_last_hip_error")
+# ... and include/rg_attn.h.
+ATTN_EXPORTS = ("rg_attn_workspace_size", "rg_attn_decode")
 
 
 def strerror(code: int) -> str:
@@ -229,3 +234,31 @@ def rg_device_cu_count():
     n = ctypes.c_int32()
     _check(lib.rg_device_cu_count(ctypes.byref(n)), "rg_device_cu_count")
     return n.value
+
+
+def rg_attn_workspace_size(B, H, Lmax, D):
+    return int(lib.rg_attn_workspace_size(B, H, Lmax, D))
+
+
+def rg_attn_decode(q, kc, vc, lens, out, scale, workspace=None, stream=None):
+    """Fixed-order decode attention: q f32 [B,H,D], kc/vc bf16 [B,Hkv,Lmax,D], lens int32 [B], out f32 [B,H,D].
+    `workspace` (a uint8 device tensor of rg_attn_workspace_size bytes) is allocated by torch if None."""
+    import torch
+    pq = _tensor_ptr(q, (torch.float32,), "q")
+    pk = _tensor_ptr(kc, (torch.bfloat16, torch.int16, torch.uint16), "kc")
+    pv = _tensor_ptr(vc, (torch.bfloat16, torch.int16, torch.uint16), "vc")
+    pl = _tensor_ptr(lens, (torch.int32,), "lens")
+    po = _tensor_ptr(out, (torch.float32,), "out")
+    if q.dim() != 3 or kc.dim() != 4 or tuple(vc.shape) != tuple(kc.shape) or tuple(out.shape) != tuple(q.shape):
+        raise ValueError("q/out [B,H,D], kc/vc [B,Hkv,Lmax,D]")
+    B, H, D = q.shape
+    _, Hkv, Lmax, D2 = kc.shape
+    if kc.shape[0] != B or D2 != D or lens.numel() != B:
+        raise ValueError(f"shape mismatch q{tuple(q.shape)} kc{tuple(kc.shape)} lens{tuple(lens.shape)}")
+    need = rg_attn_workspace_size(B, H, Lmax, D)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    pw = _tensor_ptr(workspace, (torch.uint8,), "workspace")
+    _check(lib.rg_attn_decode(pq, pk, pv, pl, po, B, H, Hkv, Lmax, D, float(scale), pw, workspace.numel(),
+                              _stream_ptr(stream)), "rg_attn_decode")
+    return out

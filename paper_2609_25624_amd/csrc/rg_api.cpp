@@ -14,6 +14,7 @@
 #include <mutex>
 
 #include "../../include/rg.h"
+#include "../../include/rg_attn.h"
 #include "rg_kernels.h"
 
 namespace {
@@ -238,6 +239,26 @@ bool stream_schedule(int64_t M, int64_t N, const rg_launch_t& o, Plan* p) {
     p->grid = (int)grid;
     p->nw = 4;
     p->rq = 2;                                    // reported as 8 rows per round
+    return true;
+}
+
+// Attention workspace: t [B][H][Lmax], segmax and spart [B][H][J], npart [B][H][J][D]
+// (float32), each region starting on a 256-byte boundary.
+struct AttnLayout {
+    int64_t t = 0, segmax = 0, spart = 0, npart = 0, total = 0;
+};
+
+bool attn_layout(int64_t B, int64_t H, int64_t Lmax, int64_t D, AttnLayout* lay) {
+    if (B < 1 || H < 1 || Lmax < 1 || D < 1 || D > 256) return false;
+    if (!mul_ok(B, H) || !mul_ok(B * H, Lmax) || !mul_ok(B * H * Lmax, 4)) return false;
+    const int64_t J = ceil_div(Lmax, 256);
+    if (!mul_ok(B * H * J, D)) return false;
+    auto round256 = [](int64_t v) { return (v + 255) / 256 * 256; };
+    lay->t = 0;
+    lay->segmax = round256(B * H * Lmax * 4);
+    lay->spart = lay->segmax + round256(B * H * J * 4);
+    lay->npart = lay->spart + round256(B * H * J * 4);
+    lay->total = lay->npart + round256(B * H * J * D * 4);
     return true;
 }
 
@@ -561,6 +582,56 @@ int linear_f32w_impl(const float* x, const float* w, float* y, int64_t M, int64_
 
 extern "C" {
 
+int64_t rg_attn_workspace_size(int64_t B, int64_t H, int64_t Lmax, int64_t D) {
+    AttnLayout lay;
+    return attn_layout(B, H, Lmax, D, &lay) ? lay.total : 0;
+}
+
+int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const int32_t* lens, float* out,
+                   int64_t B, int64_t H, int64_t Hkv, int64_t Lmax, int64_t D, float scale, void* workspace,
+                   int64_t workspace_bytes, void* stream) {
+    if (!q || !kc || !vc || !lens || !out || !workspace) return RG_ERR_INVAL;
+    if (B < 1 || H < 1 || Hkv < 1 || H % Hkv != 0 || H / Hkv > 8 || Lmax < 1) return RG_ERR_INVAL;
+    if (D < 8 || D > 256 || D % 8 != 0) return RG_ERR_INVAL;
+    AttnLayout lay;
+    if (!attn_layout(B, H, Lmax, D, &lay)) return RG_ERR_INVAL;
+    if (!mul_ok(B * Hkv, Lmax) || !mul_ok(B * Hkv * Lmax, D)) return RG_ERR_INVAL;
+    const int64_t J = ceil_div(Lmax, 256);
+    if (B * Hkv * J > 0x7fffffff || B * H > 0x7fffffff) return RG_ERR_INVAL;
+    if (workspace_bytes < lay.total) return RG_ERR_INVAL;
+    if (((uintptr_t)q & 15) || ((uintptr_t)out & 15) || ((uintptr_t)workspace & 15) || ((uintptr_t)kc & 15) ||
+        ((uintptr_t)vc & 15) || ((uintptr_t)lens & 3))
+        return RG_ERR_ALIGN;
+    const size_t qb = (size_t)(B * H * D) * 4, cb = (size_t)(B * Hkv * Lmax * D) * 2, lb = (size_t)B * 4;
+    const size_t wb = (size_t)lay.total;
+    if (overlaps(out, qb, q, qb) || overlaps(out, qb, kc, cb) || overlaps(out, qb, vc, cb) ||
+        overlaps(out, qb, lens, lb) || overlaps(out, qb, workspace, wb) || overlaps(workspace, wb, q, qb) ||
+        overlaps(workspace, wb, kc, cb) || overlaps(workspace, wb, vc, cb) || overlaps(workspace, wb, lens, lb))
+        return RG_ERR_ALIAS;
+    const int dc = device_check(nullptr);
+    if (dc != RG_OK) return dc;
+    char* ws = static_cast<char*>(workspace);
+    rg::AttnArgs a;
+    a.q = q;
+    a.k = kc;
+    a.v = vc;
+    a.lens = lens;
+    a.out = out;
+    a.t = reinterpret_cast<float*>(ws + lay.t);
+    a.segmax = reinterpret_cast<float*>(ws + lay.segmax);
+    a.spart = reinterpret_cast<float*>(ws + lay.spart);
+    a.npart = reinterpret_cast<float*>(ws + lay.npart);
+    a.B = B;
+    a.H = H;
+    a.Hkv = Hkv;
+    a.Lmax = Lmax;
+    a.D = D;
+    a.J = J;
+    a.scale = scale;
+    (void)hipGetLastError();
+    return hip_status(rg::launch_attn(a, (hipStream_t)stream));
+}
+
 int rg_linear_f32w(const float* x, const float* w, float* y, int64_t M, int64_t N, int64_t K, void* stream) {
     return linear_f32w_impl(x, w, y, M, N, K, stream);
 }
@@ -598,6 +669,7 @@ int rg_stream_create_cu_mask(const uint32_t* mask, uint32_t nwords, void** out_s
     hipStream_t s = nullptr;
     const int st = hip_status(hipExtStreamCreateWithCUMask(&s, nwords, mask));
     if (st == RG_OK) *out_stream = (void*)s;
+    else (void)hipGetLastError();   // the runtime may refuse a mask; do not leave its error for the next caller
     return st;
 }
 

@@ -16,6 +16,7 @@ _lib = None
 TID_X = 1
 TID_W = 2
 TID_B = 3
+TID_Q, TID_K, TID_V = 4, 6, 7
 
 
 def lib():
@@ -69,3 +70,13 @@ def layer_inputs(M: int, N: int, K: int, seed: int = 0, w_std: float = 0.02, lay
 def layer_bias(N: int, seed: int = 0, std: float = 0.02, layer: int = 0) -> np.ndarray:
     """float32 bias [N] ~ N(0, std^2) for one layer (a row of the same counter-based stream)."""
     return normal_f32(1, N, seed, TID_B + 16 * layer, std)[0]
+
+
+def attn_inputs(B: int, H: int, Hkv: int, Lmax: int, D: int, seed: int = 0, kstd: float = 1.0):
+    """Decode attention inputs: q f32 [B,H,D] ~ N(0,1); key and value caches as bfloat16 bits
+    [B,Hkv,Lmax,D], keys ~ N(0, kstd^2), values ~ N(0,1).  Row r of a cache is position r % Lmax
+    of sequence-head r // Lmax, so a shorter Lmax is not a prefix; callers slice instead."""
+    q = normal_f32(B * H, D, seed, TID_Q, 1.0).reshape(B, H, D)
+    k = normal_bf16(B * Hkv * Lmax, D, seed, TID_K, kstd).reshape(B, Hkv, Lmax, D)
+    v = normal_bf16(B * Hkv * Lmax, D, seed, TID_V, 1.0).reshape(B, Hkv, Lmax, D)
+    return q, k, v

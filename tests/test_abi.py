@@ -202,3 +202,49 @@ def test_f32w_planner_and_argument_checks():
     assert L.rg_linear_f32w(0x1000, 0x2002, 0x3000, 1, 1, 1, None) == rg.RG_ERR_ALIGN
     assert L.rg_linear_f32w(0x1000, 0x2000, 0x1000, 1, 1, 1, None) == rg.RG_ERR_ALIAS
     assert L.rg_linear_f32w(0x1000, 0x2000, 0x3000, 1, 0, 1, None) == rg.RG_ERR_INVAL
+
+
+def test_attention_header_exports_and_host_checks():
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "rg_attn.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"^\s*(?:int|int64_t)\s+(rg_\w+)\s*\(", text, flags=re.M)))
+    assert sorted(rg.ATTN_EXPORTS) == names
+    lib = ctypes.CDLL(rg.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    ws = rg.rg_attn_workspace_size(16, 32, 4096, 128)
+    assert ws >= 4 * (16 * 32 * 4096 + 2 * 16 * 32 * 16 + 16 * 32 * 16 * 128)
+    assert rg.rg_attn_workspace_size(0, 32, 4096, 128) == 0
+    L = rg.lib
+    a = 0x100000
+    # null, bad group, bad D, small workspace, misalignment -- all before any device call
+    assert L.rg_attn_decode(None, a, a, a, a, 1, 1, 1, 16, 64, 1.0, a, 1 << 20, None) == rg.RG_ERR_INVAL
+    assert L.rg_attn_decode(a, a, a, a, a, 1, 3, 2, 16, 64, 1.0, a, 1 << 20, None) == rg.RG_ERR_INVAL
+    assert L.rg_attn_decode(a, a, a, a, a, 1, 9, 1, 16, 64, 1.0, a, 1 << 20, None) == rg.RG_ERR_INVAL
+    assert L.rg_attn_decode(a, a, a, a, a, 1, 1, 1, 16, 60, 1.0, a, 1 << 20, None) == rg.RG_ERR_INVAL
+    assert L.rg_attn_decode(a, a, a, a, a, 1, 1, 1, 16, 264, 1.0, a, 1 << 20, None) == rg.RG_ERR_INVAL
+    assert L.rg_attn_decode(a, a, a, a, a, 1, 1, 1, 16, 64, 1.0, a, 8, None) == rg.RG_ERR_INVAL
+    assert L.rg_attn_decode(a + 4, a, a, a, 0x900000, 1, 1, 1, 16, 64, 1.0, 0xA00000, 1 << 20, None) == rg.RG_ERR_ALIGN
+    assert L.rg_attn_decode(0x100000, 0x200000, 0x300000, 0x400000, 0x100000, 1, 1, 1, 16, 64, 1.0, 0xA00000,
+                            1 << 20, None) == rg.RG_ERR_ALIAS
+
+
+def test_attention_kernels_use_only_ieee_operations():
+    import subprocess
+    import tempfile
+    from paper_2609_25624_amd import build as b
+    src = os.path.join(ROOT, "paper_2609_25624_amd", "csrc", "rg_attn.hip")
+    code = re.sub(r"//.*", "", open(src).read())
+    for bad in ("atomic", "mfma", "__expf", "__builtin_expf", "exp2f", "fast-math"):
+        assert bad not in code, bad
+    with tempfile.TemporaryDirectory() as d:
+        out = os.path.join(d, "a.s")
+        r = subprocess.run([b.HIPCC, "-x", "hip", *b.COMMON, *b.DEVICE, "--cuda-device-only", "-S", src, "-o", out],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+        asm = open(out).read()
+    insts = set(re.findall(r"^\s+(v_[a-z0-9_]+)", asm, flags=re.M))
+    for i in insts:
+        assert not re.match(r"v_(mfma|dot\d|pk_(fma|mul|add)_f32|mad_f32|mac_f32|exp_f32|log_f32|fma_mix|mad_mix)", i), i
+    assert "v_div_fixup_f32" in insts          # the correctly rounded division
+    modes = re.findall(r"\.amdhsa_float_denorm_mode_32\s+(\d+)", asm)
+    assert modes and set(modes) == {"3"}
