@@ -242,10 +242,10 @@ bool stream_schedule(int64_t M, int64_t N, const rg_launch_t& o, Plan* p) {
     return true;
 }
 
-// Attention workspace: t [B][H][Lmax], segmax and spart [B][H][J], npart [B][H][J][D]
+// Attention workspace: t [B][H][Lmax], segmax and spart [B][H][J], mmax [B][H], npart [B][H][J][D]
 // (float32), each region starting on a 256-byte boundary.
 struct AttnLayout {
-    int64_t t = 0, segmax = 0, spart = 0, npart = 0, total = 0;
+    int64_t t = 0, segmax = 0, spart = 0, mmax = 0, npart = 0, total = 0;
 };
 
 bool attn_layout(int64_t B, int64_t H, int64_t Lmax, int64_t D, AttnLayout* lay) {
@@ -257,7 +257,8 @@ bool attn_layout(int64_t B, int64_t H, int64_t Lmax, int64_t D, AttnLayout* lay)
     lay->t = 0;
     lay->segmax = round256(B * H * Lmax * 4);
     lay->spart = lay->segmax + round256(B * H * J * 4);
-    lay->npart = lay->spart + round256(B * H * J * 4);
+    lay->mmax = lay->spart + round256(B * H * J * 4);
+    lay->npart = lay->mmax + round256(B * H * 4);
     lay->total = lay->npart + round256(B * H * J * D * 4);
     return true;
 }
@@ -597,7 +598,7 @@ int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const
     if (!attn_layout(B, H, Lmax, D, &lay)) return RG_ERR_INVAL;
     if (!mul_ok(B * Hkv, Lmax) || !mul_ok(B * Hkv * Lmax, D)) return RG_ERR_INVAL;
     const int64_t J = ceil_div(Lmax, 256);
-    if (B * Hkv * J > 0x7fffffff || B * H > 0x7fffffff) return RG_ERR_INVAL;
+    if (B * Hkv * J > 0x3fffffff || B * H > 0x7fffffff) return RG_ERR_INVAL;   // work items fit int32
     if (workspace_bytes < lay.total) return RG_ERR_INVAL;
     if (((uintptr_t)q & 15) || ((uintptr_t)out & 15) || ((uintptr_t)workspace & 15) || ((uintptr_t)kc & 15) ||
         ((uintptr_t)vc & 15) || ((uintptr_t)lens & 3))
@@ -608,7 +609,8 @@ int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const
         overlaps(out, qb, lens, lb) || overlaps(out, qb, workspace, wb) || overlaps(workspace, wb, q, qb) ||
         overlaps(workspace, wb, kc, cb) || overlaps(workspace, wb, vc, cb) || overlaps(workspace, wb, lens, lb))
         return RG_ERR_ALIAS;
-    const int dc = device_check(nullptr);
+    int cus = 0;
+    const int dc = device_check(&cus);
     if (dc != RG_OK) return dc;
     char* ws = static_cast<char*>(workspace);
     rg::AttnArgs a;
@@ -620,6 +622,7 @@ int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const
     a.t = reinterpret_cast<float*>(ws + lay.t);
     a.segmax = reinterpret_cast<float*>(ws + lay.segmax);
     a.spart = reinterpret_cast<float*>(ws + lay.spart);
+    a.mmax = reinterpret_cast<float*>(ws + lay.mmax);
     a.npart = reinterpret_cast<float*>(ws + lay.npart);
     a.B = B;
     a.H = H;
@@ -628,8 +631,10 @@ int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const
     a.D = D;
     a.J = J;
     a.scale = scale;
+    const uint64_t vpr = (uint64_t)(D / 8);
+    a.vmagic = vpr > 1 ? (uint32_t)((((uint64_t)1 << 32) + vpr - 1) / vpr) : 0u;
     (void)hipGetLastError();
-    return hip_status(rg::launch_attn(a, (hipStream_t)stream));
+    return hip_status(rg::launch_attn(a, cus, (hipStream_t)stream));
 }
 
 int rg_linear_f32w(const float* x, const float* w, float* y, int64_t M, int64_t N, int64_t K, void* stream) {

@@ -1,21 +1,24 @@
 // Fixed-order decode attention kernels for gfx950 (MI355X): the order
 // RG-ATTN-1 and its exponential EXP1, both defined in include/rg_attn.h.
 //
-// Three launches, each deterministic by construction (no atomics, no order
+// Four launches, each deterministic by construction (no atomics, no order
 // that depends on the grid):
-//   1. scores:   workgroup (b, g, j) stages the keys of positions
-//                [256j, 256j + 256) of kv head g in LDS; thread l runs the dot
-//                product chain of position l for every query head of the
-//                group, scales it, writes t, and the workgroup writes the
-//                segment's maximum per head (max is exact, so its tree shape
-//                does not matter).
-//   2. partials: workgroup (b, g, j) takes m = the maximum of the segment
-//                maxima, computes e_l = EXP1(t_l - m) for its positions, the
-//                segment sum S_j (one sequential chain per head) and the
-//                segment numerators n_j[d] (one fmaf chain per head and d over
-//                the positions in ascending order, values staged in LDS).
-//   3. fold:     workgroup (b, h) folds the S_j and n_j[d] in ascending j and
+//   1. scores:   work item (b, g, j) = segment j (positions [256j, 256j + 256))
+//                of kv head g of sequence b; its keys are staged in LDS and
+//                thread l runs the dot product chain of position l for every
+//                query head of the group, scales it, writes t, and the
+//                workgroup writes the segment's maximum per head (max is
+//                exact, so its tree shape does not matter).
+//   2. max:      m[b][h] = the largest segment maximum.
+//   3. partials: per work item, e_l = EXP1(t_l - m), the segment sum S_j (one
+//                addition chain per head) and the segment numerators n_j[d]
+//                (one fmaf chain per head and d over the positions in
+//                ascending order; values and e staged in LDS).
+//   4. fold:     workgroup (b, h) folds the S_j and n_j[d] in ascending j and
 //                divides.
+// Kernels 1 and 3 are persistent: a workgroup walks work items it, it + grid,
+// ... in steps of one 32 KB tile (for the usual head dims), and fetches the next
+// step's tile into registers while it computes the current one from LDS.
 // Arithmetic: binary32 fmaf / add / multiply / correctly rounded divide,
 // denormals kept, no contraction (the build uses -ffp-contract=off).
 
@@ -54,151 +57,334 @@ __device__ __forceinline__ int clamp_len(const int32_t* lens, int64_t b, int64_t
     return (int)(L < 0 ? 0 : (L > Lmax ? Lmax : L));
 }
 
-// Stage rows [0, rows) of a [*, D] bf16 block (contiguous) into LDS at a row
-// stride of D + 8 (16 bytes of pad: the lanes that read one row each hit
-// different banks).  D % 8 == 0.
-__device__ __forceinline__ void stage_rows(const uint16_t* __restrict__ src, uint16_t* dst, int rows, int D) {
-    const int vpr = D / 8;                    // 16-byte vectors per row
-    const int total = rows * vpr;
-    for (int i = threadIdx.x; i < total; i += blockDim.x) {
-        const int r = i / vpr, c = i % vpr;
-        *reinterpret_cast<uint4*>(dst + r * (D + 8) + 8 * c) = *reinterpret_cast<const uint4*>(src + (int64_t)r * D + 8 * c);
+// A step's tile: `rows` rows of VPR 16-byte vectors (8 bf16 each) taken from a
+// [*, D] bf16 block at row stride D, staged in LDS at a row stride of
+// 8 * VPR + 8 (16 bytes of pad: lanes that read one row each hit different
+// banks).  It is fetched into registers one step ahead (every load issued
+// before the first use) and stored to LDS between barriers; rows past the
+// sequence are +0.  Thread t holds vectors t, t + 256, ...; the row of vector i
+// is i / VPR (a shift for the fixed shapes, else a multiply by `vmagic` =
+// ceil(2^32 / vpr), exact for i < 8192).
+template <int NV, int VPR>   // VPR > 0: fixed vectors per row; 0: vpr at run time
+struct Tile {
+    uint4 r[NV];
+    __device__ __forceinline__ static int row_of(int i, int vpr, uint32_t vmagic) {
+        if constexpr (VPR > 0) return i / VPR;
+        return vpr == 1 ? i : (int)__umulhi((uint32_t)i, vmagic);
+    }
+    __device__ __forceinline__ void fetch(const uint16_t* __restrict__ src, int64_t stride, int rows, int vpr,
+                                          uint32_t vmagic) {
+        if constexpr (VPR > 0) vpr = VPR;
+        const int limit = rows * vpr;
+#pragma unroll
+        for (int u = 0; u < NV; ++u) {
+            const int i = (int)threadIdx.x + 256 * u;
+            const int row = row_of(i, vpr, vmagic);
+            r[u] = i < limit ? *reinterpret_cast<const uint4*>(src + row * stride + 8 * (i - row * vpr))
+                             : make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+    __device__ __forceinline__ void store(uint16_t* dst, int rows_total, int vpr, uint32_t vmagic) const {
+        if constexpr (VPR > 0) vpr = VPR;
+#pragma unroll
+        for (int u = 0; u < NV; ++u) {
+            const int i = (int)threadIdx.x + 256 * u;
+            if (VPR > 0 || i < rows_total * vpr) {
+                const int row = row_of(i, vpr, vmagic);
+                *reinterpret_cast<uint4*>(dst + 8 * (i + row)) = r[u];   // row * (8 vpr + 8) + 8 (i % vpr)
+            }
+        }
+    }
+};
+
+// Work item it = (b * Hkv + g) * J + j: segment j of kv head g of sequence b.
+struct Item {
+    int b, g, j;
+    int L, l0, rows;
+};
+
+__device__ __forceinline__ Item item_of(const AttnArgs& a, int it) {
+    Item w;
+    const int J = (int)a.J, Hkv = (int)a.Hkv;
+    const int bg = it / J;
+    w.j = it - bg * J;
+    w.b = bg / Hkv;
+    w.g = bg - w.b * Hkv;
+    w.L = clamp_len(a.lens, w.b, a.Lmax);
+    w.l0 = w.j * kAttnSeg;
+    w.rows = w.L - w.l0 < kAttnSeg ? w.L - w.l0 : kAttnSeg;
+    return w;
+}
+
+// The first item at or after `it`, stepping by the grid, that holds positions.
+__device__ __forceinline__ int next_item(const AttnArgs& a, int it, int items) {
+    while (it < items && item_of(a, it).rows <= 0) it += (int)gridDim.x;
+    return it;
+}
+
+typedef const __attribute__((address_space(4))) float cfloat;   // read-only: uniform loads go to SGPRs
+
+// Exact maximum over the workgroup of one value per thread: lanes by xor
+// shuffles, then the four waves through LDS (fmaxf is exact and NaN never
+// wins, so any tree gives the same value).
+template <int G>
+__device__ __forceinline__ void block_max(float (&v)[G], float (*wred)[G]) {
+#pragma unroll
+    for (int sh = 32; sh > 0; sh >>= 1)
+#pragma unroll
+        for (int i = 0; i < G; ++i) v[i] = __builtin_fmaxf(v[i], __shfl_xor(v[i], sh, 64));
+    if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+        for (int i = 0; i < G; ++i) wred[threadIdx.x >> 6][i] = v[i];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+        v[i] = __builtin_fmaxf(__builtin_fmaxf(wred[0][i], wred[1][i]), __builtin_fmaxf(wred[2][i], wred[3][i]));
+}
+
+// 1. scores and segment maxima.  Work item = segment; its NC steps take the keys'
+// columns [c DC, c DC + DC) in turn (DC = 64 for the fixed head dims, else DC = D
+// in one step), so each thread's dot product chain of position l continues across
+// the steps in ascending d.  G query heads per kv head, their chains interleaved;
+// q is read with uniform (scalar) loads.
+template <int G, int DC, int NC, bool EXACT>
+__global__ void __launch_bounds__(256) attn_scores_kernel(AttnArgs a) {
+    constexpr int VPR = EXACT ? DC / 8 : 0;
+    constexpr int NV = DC / 8;                                                // vectors per thread (256 rows)
+    __shared__ __attribute__((aligned(16))) uint16_t ks[kAttnSeg * (DC + 8)]; // [256][DC + 8]
+    __shared__ float wred[4][G];
+    const int D = EXACT ? DC * NC : (int)a.D, l = threadIdx.x;
+    const int dc = EXACT ? DC : D;                    // columns per step
+    const int vpr = dc / 8;
+    const int items = (int)(a.B * a.Hkv * a.J);
+    cfloat* q4 = (cfloat*)a.q;
+    Tile<NV, VPR> tile;
+    auto fetch = [&](const Item& w, int c) {
+        tile.fetch(a.k + (((int64_t)w.b * a.Hkv + w.g) * a.Lmax + w.l0) * D + c * dc, D, w.rows, vpr, a.vmagic);
+    };
+    int it = next_item(a, (int)blockIdx.x, items);
+    Item w;
+    int c = 0;
+    if (it < items) {
+        w = item_of(a, it);
+        fetch(w, 0);
+    }
+    float z[G];
+    while (it < items) {
+        __syncthreads();                              // the previous step's reads of LDS are done
+        tile.store(ks, kAttnSeg, vpr, a.vmagic);
+        __syncthreads();
+        const Item cur = w;
+        const int cc = c;
+        if (c + 1 < NC) {
+            ++c;
+        } else {
+            c = 0;
+            it = next_item(a, it + (int)gridDim.x, items);
+            if (it < items) w = item_of(a, it);
+        }
+        if (it < items) fetch(w, c);                  // in flight during this step's chains
+        if (cc == 0) {
+#pragma unroll
+            for (int i = 0; i < G; ++i) z[i] = 0.0f;
+        }
+        const int64_t h0 = (int64_t)cur.g * G;
+        const int64_t qbase = ((int64_t)cur.b * a.H + h0) * D + cc * dc;
+        if (l < cur.rows) {
+            const uint16_t* kr = ks + l * (dc + 8);
+#pragma unroll 4
+            for (int d = 0; d < DC; d += 8) {
+                if (!EXACT && d >= dc) break;
+                const uint4 kv = *reinterpret_cast<const uint4*>(kr + d);
+                const uint32_t w4[4] = {kv.x, kv.y, kv.z, kv.w};
+                float kf[8];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    kf[2 * e] = __uint_as_float(w4[e] << 16);
+                    kf[2 * e + 1] = __uint_as_float(w4[e] & 0xffff0000u);
+                }
+#pragma unroll
+                for (int i = 0; i < G; ++i)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) z[i] = __builtin_fmaf(q4[qbase + i * D + d + e], kf[e], z[i]);
+            }
+        }
+        if (cc == NC - 1) {
+            float t[G];
+#pragma unroll
+            for (int i = 0; i < G; ++i) {
+                t[i] = l < cur.rows ? z[i] * a.scale : -__builtin_inff();
+                if (l < cur.rows) a.t[(((int64_t)cur.b * a.H + h0 + i) * a.Lmax) + cur.l0 + l] = t[i];
+            }
+            block_max<G>(t, wred);
+            float mine = t[0];                        // thread l < G writes head l's maximum
+#pragma unroll
+            for (int i = 1; i < G; ++i) mine = (l == i) ? t[i] : mine;
+            if (l < G) a.segmax[((int64_t)cur.b * a.H + h0 + l) * a.J + cur.j] = mine;
+        }
     }
 }
 
-// G query heads per kv head; DM >= D bounds the LDS tiles (64, 128 or 256).
-template <int G, int DM>
-__global__ void __launch_bounds__(256) attn_scores_kernel(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) float qs[G * DM];                 // [G][D]
-    __shared__ __attribute__((aligned(16))) uint16_t ks[kAttnSeg * (DM + 8)]; // [256][D + 8]
-    __shared__ float red[G][256];
-    const int D = a.D;
-
-    const int64_t j = blockIdx.x % a.J, bg = blockIdx.x / a.J;
-    const int64_t b = bg / a.Hkv, g = bg % a.Hkv;
-    const int L = clamp_len(a.lens, b, a.Lmax);
-    const int l0 = (int)(j * kAttnSeg);
-    if (l0 >= L) return;                          // the whole workgroup: no barrier below is skipped by part of it
-    const int rows = min(kAttnSeg, L - l0);
-    const int64_t h0 = g * G;
-    for (int i = threadIdx.x; i < G * D; i += blockDim.x) qs[i] = a.q[(b * a.H + h0) * D + i];
-    stage_rows(a.k + ((b * a.Hkv + g) * a.Lmax + l0) * D, ks, rows, D);
-    __syncthreads();
-
-    const int l = threadIdx.x;
-    float t[G];
-    if (l < rows) {
-        float z[G];
+// 2. m[b][h] = the largest segment maximum (exact).  One thread per (b, h).
+__global__ void __launch_bounds__(256) attn_max_kernel(AttnArgs a) {
+    const int64_t bh = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (bh >= a.B * a.H) return;
+    const int L = clamp_len(a.lens, bh / a.H, a.Lmax);
+    const int Jb = (L + kAttnSeg - 1) / kAttnSeg;
+    const float* sm = a.segmax + bh * a.J;
+    float m = -__builtin_inff();
+    int jj = 0;
+    for (; jj + 8 <= Jb; jj += 8) {
+        float v[8];
 #pragma unroll
-        for (int i = 0; i < G; ++i) z[i] = 0.0f;
-        const uint16_t* kr = ks + l * (D + 8);
-        for (int d = 0; d < D; d += 8) {
-            const uint4 kv = *reinterpret_cast<const uint4*>(kr + d);
-            const uint32_t w4[4] = {kv.x, kv.y, kv.z, kv.w};
-            float kf[8];
+        for (int i = 0; i < 8; ++i) v[i] = sm[jj + i];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                kf[2 * e] = __uint_as_float(w4[e] << 16);
-                kf[2 * e + 1] = __uint_as_float(w4[e] & 0xffff0000u);
-            }
-#pragma unroll
-            for (int i = 0; i < G; ++i)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) z[i] = __builtin_fmaf(qs[i * D + d + e], kf[e], z[i]);
-        }
-#pragma unroll
-        for (int i = 0; i < G; ++i) {
-            t[i] = z[i] * a.scale;
-            a.t[((b * a.H + h0 + i) * a.Lmax) + l0 + l] = t[i];
-        }
-    } else {
-#pragma unroll
-        for (int i = 0; i < G; ++i) t[i] = -__builtin_inff();
+        for (int i = 0; i < 8; ++i) m = __builtin_fmaxf(m, v[i]);
     }
-    // segment maximum per head: a fixed tree of fmaxf (exact; NaN never wins)
+    for (; jj < Jb; ++jj) m = __builtin_fmaxf(m, sm[jj]);
+    a.mmax[bh] = m;
+}
+
+// 3. exponentials and the segment partials S_j and n_j[d].  Work item = segment;
+// its NS steps take positions [l0 + s RS, l0 + s RS + RS) in turn (RS = 16384 / D
+// rows for the fixed head dims, else all 256 in one step), so every chain below
+// continues across the steps in ascending l.  e for the segment is computed at
+// its first step into LDS ([head][position], +0 past the sequence).  Unit u =
+// (head, pair of adjacent d): two fmaf chains over the positions; threads tid < G
+// also run the segment sum of head tid (an addition chain).  Chains run over all
+// 256 positions of the segment: past the sequence e = +0 and the values are +0,
+// and adding +0 to a chain that starts at +0 and never becomes -0 changes no bit.
+template <int G, int DM, int RS, bool EXACT>
+__global__ void __launch_bounds__(256) attn_partials_kernel(AttnArgs a) {
+    constexpr int NS = kAttnSeg / RS;                 // steps per item
+    constexpr int VPR = EXACT ? DM / 8 : 0;
+    constexpr int NV = RS * DM / 8 / 256;             // vectors per thread
+    constexpr int UPT = (G * DM / 2 + 255) / 256;     // units per thread
+    __shared__ __attribute__((aligned(16))) float es[G * kAttnSeg];           // [G][256]
+    __shared__ __attribute__((aligned(16))) uint16_t vs[RS * (DM + 8)];       // [RS][D + 8]
+    const int D = EXACT ? DM : (int)a.D, tid = threadIdx.x;
+    const int vpr = D / 8;
+    const int items = (int)(a.B * a.Hkv * a.J);
+    Tile<NV, VPR> tile;
+    float tr[G], mr[G];
+    auto fetch = [&](const Item& w, int s) {
+        const int r0 = s * RS;
+        const int rows = w.rows - r0 < RS ? w.rows - r0 : RS;
+        tile.fetch(a.v + (((int64_t)w.b * a.Hkv + w.g) * a.Lmax + w.l0 + r0) * D, D, rows, vpr, a.vmagic);
+        if (s == 0) {
+            const int64_t h0 = (int64_t)w.g * G;
 #pragma unroll
-    for (int i = 0; i < G; ++i) red[i][l] = t[i];
-    __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
-        if (l < s) {
+            for (int i = 0; i < G; ++i) {
+                tr[i] = tid < w.rows ? a.t[((int64_t)w.b * a.H + h0 + i) * a.Lmax + w.l0 + tid] : 0.0f;
+                mr[i] = a.mmax[(int64_t)w.b * a.H + h0 + i];
+            }
+        }
+    };
+    int it = next_item(a, (int)blockIdx.x, items);
+    Item w;
+    int st = 0;
+    if (it < items) {
+        w = item_of(a, it);
+        fetch(w, 0);
+    }
+    const int npd = D / 2;
+    const int nunits = G * npd;
+    float n0[UPT], n1[UPT], ssum = 0.0f;
+    while (it < items) {
+        __syncthreads();
+        tile.store(vs, RS, vpr, a.vmagic);
+        if (st == 0) {
 #pragma unroll
-            for (int i = 0; i < G; ++i) red[i][l] = __builtin_fmaxf(red[i][l], red[i][l + s]);
+            for (int i = 0; i < G; ++i) es[i * kAttnSeg + tid] = tid < w.rows ? exp1(tr[i] - mr[i]) : 0.0f;
         }
         __syncthreads();
+        const Item cur = w;
+        const int ss = st;
+        if (st + 1 < NS) {
+            ++st;
+        } else {
+            st = 0;
+            it = next_item(a, it + (int)gridDim.x, items);
+            if (it < items) w = item_of(a, it);
+        }
+        if (it < items) fetch(w, st);                 // in flight during this step's chains
+        if (ss == 0) {
+#pragma unroll
+            for (int k = 0; k < UPT; ++k) n0[k] = n1[k] = 0.0f;
+            ssum = 0.0f;
+        }
+        const int lb = ss * RS;                        // first position of this step in the segment
+#pragma unroll
+        for (int k = 0; k < UPT; ++k) {
+            const int u = tid + 256 * k;
+            if (u < nunits) {
+                const int hh = u / npd, d = 2 * (u - hh * npd);
+                const bool sums = k == 0 && tid < G;
+                const float* ep = es + hh * kAttnSeg + lb;
+                const float* sp = es + (tid < G ? tid : 0) * kAttnSeg + lb;
+                const uint16_t* vp = vs + d;
+                float x0 = n0[k], x1 = n1[k], sm = ssum;
+#pragma unroll 2
+                for (int l = 0; l < RS; l += 8) {
+                    const float4 e0 = *reinterpret_cast<const float4*>(ep + l);
+                    const float4 e1 = *reinterpret_cast<const float4*>(ep + l + 4);
+                    const float ev[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
+                    uint32_t vv[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) vv[i] = *reinterpret_cast<const uint32_t*>(vp + (l + i) * (D + 8));
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        x0 = __builtin_fmaf(ev[i], __uint_as_float(vv[i] << 16), x0);
+                        x1 = __builtin_fmaf(ev[i], __uint_as_float(vv[i] & 0xffff0000u), x1);
+                    }
+                    if (sums) {
+                        const float4 s0 = *reinterpret_cast<const float4*>(sp + l);
+                        const float4 s1 = *reinterpret_cast<const float4*>(sp + l + 4);
+                        sm = sm + s0.x; sm = sm + s0.y; sm = sm + s0.z; sm = sm + s0.w;
+                        sm = sm + s1.x; sm = sm + s1.y; sm = sm + s1.z; sm = sm + s1.w;
+                    }
+                }
+                n0[k] = x0;
+                n1[k] = x1;
+                if (sums) ssum = sm;
+                if (ss == NS - 1) {
+                    float* np = a.npart + (((int64_t)cur.b * a.H + cur.g * G + hh) * a.J + cur.j) * D + d;
+                    np[0] = x0;
+                    np[1] = x1;
+                    if (sums) a.spart[((int64_t)cur.b * a.H + cur.g * G + tid) * a.J + cur.j] = sm;
+                }
+            }
+        }
     }
-    if (l < G) a.segmax[(b * a.H + h0 + l) * a.J + j] = red[l][0];
 }
 
-template <int G, int DM>
-__global__ void __launch_bounds__(256) attn_partials_kernel(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) float es[G * kAttnSeg];           // [G][256]
-    __shared__ __attribute__((aligned(16))) uint16_t vs[kAttnSeg * (DM + 8)]; // [256][D + 8]
-    __shared__ float mh[G];
-    const int D = a.D;
-
-    const int64_t j = blockIdx.x % a.J, bg = blockIdx.x / a.J;
-    const int64_t b = bg / a.Hkv, g = bg % a.Hkv;
-    const int L = clamp_len(a.lens, b, a.Lmax);
-    const int l0 = (int)(j * kAttnSeg);
-    if (l0 >= L) return;
-    const int rows = min(kAttnSeg, L - l0);
-    const int Jb = (L + kAttnSeg - 1) / kAttnSeg;
-    const int64_t h0 = g * G;
-    const int tid = threadIdx.x;
-    stage_rows(a.v + ((b * a.Hkv + g) * a.Lmax + l0) * D, vs, rows, D);
-    if (tid < G) {
-        const float* sm = a.segmax + (b * a.H + h0 + tid) * a.J;
-        float m = sm[0];
-        for (int jj = 1; jj < Jb; ++jj) m = __builtin_fmaxf(m, sm[jj]);
-        mh[tid] = m;
-    }
-    __syncthreads();
-    if (tid < rows) {
-#pragma unroll
-        for (int i = 0; i < G; ++i)
-            es[i * kAttnSeg + tid] = exp1(a.t[(b * a.H + h0 + i) * a.Lmax + l0 + tid] - mh[i]);
-    }
-    __syncthreads();
-    // segment sums: one sequential chain per head
-    if (tid < G) {
-        float s = 0.0f;
-        for (int l = 0; l < rows; ++l) s = s + es[tid * kAttnSeg + l];
-        a.spart[(b * a.H + h0 + tid) * a.J + j] = s;
-    }
-    // segment numerators: thread handles (head, d) pairs p = tid, tid + 256, ... as independent chains
-    constexpr int kMaxPairs = (G * DM + 255) / 256;
-    const int npairs = G * D;
-    float n[kMaxPairs];
-    int hh[kMaxPairs], dd[kMaxPairs];
-#pragma unroll
-    for (int u = 0; u < kMaxPairs; ++u) {
-        const int p = tid + 256 * u;
-        hh[u] = p < npairs ? p / D : 0;
-        dd[u] = p < npairs ? p % D : 0;
-        n[u] = 0.0f;
-    }
-    const int nu = (npairs - tid + 255) / 256;       // pairs of this thread
-    for (int l = 0; l < rows; ++l) {
-        const uint16_t* vr = vs + l * (D + 8);
-#pragma unroll
-        for (int u = 0; u < kMaxPairs; ++u)
-            if (u < nu) n[u] = __builtin_fmaf(es[hh[u] * kAttnSeg + l], up_bf16(vr[dd[u]]), n[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < kMaxPairs; ++u)
-        if (u < nu) a.npart[((b * a.H + h0 + hh[u]) * a.J + j) * D + dd[u]] = n[u];
-}
-
+// 4. out = N / S after the ascending folds of the segment partials.  Workgroup (b, h),
+// thread d.
 __global__ void __launch_bounds__(256) attn_fold_kernel(AttnArgs a) {
     const int64_t bh = blockIdx.x, b = bh / a.H;
     const int L = clamp_len(a.lens, b, a.Lmax);
     const int Jb = (L + kAttnSeg - 1) / kAttnSeg;
     const int D = a.D;
+    const float* sp = a.spart + bh * a.J;
     for (int d = threadIdx.x; d < D; d += blockDim.x) {
-        float S = 0.0f, N = 0.0f;
-        const float* sp = a.spart + bh * a.J;
         const float* np = a.npart + bh * a.J * D + d;
-        for (int jj = 0; jj < Jb; ++jj) {
+        float S = 0.0f, N = 0.0f;
+        int jj = 0;
+        for (; jj + 8 <= Jb; jj += 8) {            // loads issued in groups, additions in order
+            float sv[8], nv[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                sv[i] = sp[jj + i];
+                nv[i] = np[(int64_t)(jj + i) * D];
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                S = (jj + i == 0) ? sv[i] : S + sv[i];
+                N = (jj + i == 0) ? nv[i] : N + nv[i];
+            }
+        }
+        for (; jj < Jb; ++jj) {
             S = (jj == 0) ? sp[0] : S + sp[jj];
             N = (jj == 0) ? np[0] : N + np[(int64_t)jj * D];
         }
@@ -206,39 +392,71 @@ __global__ void __launch_bounds__(256) attn_fold_kernel(AttnArgs a) {
     }
 }
 
-template <int G, int DM>
-hipError_t launch_group(const AttnArgs& a, hipStream_t stream) {
-    const int64_t wgs = a.B * a.Hkv * a.J;
-    hipLaunchKernelGGL((attn_scores_kernel<G, DM>), dim3((unsigned)wgs), dim3(256), 0, stream, a);
+// Workgroups each kernel keeps resident per CU: LDS-limited (160 KB per CU).
+constexpr int64_t kLdsPerCU = 160 * 1024;
+
+// Persistent grids: as many workgroups as the LDS of the device keeps resident.
+template <typename K1, typename K3>
+hipError_t launch_pair(K1 k1, int64_t lds1, K3 k3, int64_t lds3, const AttnArgs& a, int cus, hipStream_t stream) {
+    const int64_t items = a.B * a.Hkv * a.J;
+    const int64_t g1 = items < (kLdsPerCU / lds1) * cus ? items : (kLdsPerCU / lds1) * cus;
+    const int64_t g3 = items < (kLdsPerCU / lds3) * cus ? items : (kLdsPerCU / lds3) * cus;
+    hipLaunchKernelGGL(k1, dim3((unsigned)g1), dim3(256), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_partials_kernel<G, DM>), dim3((unsigned)wgs), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(attn_max_kernel, dim3((unsigned)((a.B * a.H + 255) / 256)), dim3(256), 0, stream, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k3, dim3((unsigned)g3), dim3(256), 0, stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(attn_fold_kernel, dim3((unsigned)(a.B * a.H)), dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 
+// Fixed head dims (64, 128, 256): 64-column key steps and 16384 / D-row value steps
+// (32 KB tiles, four workgroups per CU).  Other D <= DM: one step of the whole segment.
+template <int G, int D>
+hipError_t launch_fixed(const AttnArgs& a, int cus, hipStream_t stream) {
+    constexpr int RS = 16384 / D;
+    const int64_t lds1 = (int64_t)kAttnSeg * (64 + 8) * 2 + 16 * G;
+    const int64_t lds3 = (int64_t)G * kAttnSeg * 4 + (int64_t)RS * (D + 8) * 2;
+    return launch_pair(attn_scores_kernel<G, 64, D / 64, true>, lds1, attn_partials_kernel<G, D, RS, true>, lds3, a,
+                       cus, stream);
+}
+
+template <int G, int DM>
+hipError_t launch_any(const AttnArgs& a, int cus, hipStream_t stream) {
+    const int64_t lds1 = (int64_t)kAttnSeg * (DM + 8) * 2 + 16 * G;
+    const int64_t lds3 = (int64_t)G * kAttnSeg * 4 + (int64_t)kAttnSeg * (DM + 8) * 2;
+    return launch_pair(attn_scores_kernel<G, DM, 1, false>, lds1, attn_partials_kernel<G, DM, kAttnSeg, false>, lds3,
+                       a, cus, stream);
+}
+
 template <int G>
-hipError_t launch_dm(const AttnArgs& a, hipStream_t stream) {
-    if (a.D <= 64) return launch_group<G, 64>(a, stream);
-    if (a.D <= 128) return launch_group<G, 128>(a, stream);
-    return launch_group<G, 256>(a, stream);
+hipError_t launch_dm(const AttnArgs& a, int cus, hipStream_t stream) {
+    if (a.D == 64) return launch_fixed<G, 64>(a, cus, stream);
+    if (a.D == 128) return launch_fixed<G, 128>(a, cus, stream);
+    if (a.D == 256) return launch_fixed<G, 256>(a, cus, stream);
+    if (a.D <= 64) return launch_any<G, 64>(a, cus, stream);
+    if (a.D <= 128) return launch_any<G, 128>(a, cus, stream);
+    return launch_any<G, 256>(a, cus, stream);
 }
 
 }  // namespace
 
-hipError_t launch_attn(const AttnArgs& a, hipStream_t stream) {
+hipError_t launch_attn(const AttnArgs& a, int cus, hipStream_t stream) {
+    if (cus < 1) cus = 1;
     if (a.D < 8 || a.D > 256 || a.D % 8 != 0 || a.Hkv < 1 || a.H % a.Hkv != 0) return hipErrorInvalidValue;
     switch (a.H / a.Hkv) {
-        case 1: return launch_dm<1>(a, stream);
-        case 2: return launch_dm<2>(a, stream);
-        case 3: return launch_dm<3>(a, stream);
-        case 4: return launch_dm<4>(a, stream);
-        case 5: return launch_dm<5>(a, stream);
-        case 6: return launch_dm<6>(a, stream);
-        case 7: return launch_dm<7>(a, stream);
-        case 8: return launch_dm<8>(a, stream);
+        case 1: return launch_dm<1>(a, cus, stream);
+        case 2: return launch_dm<2>(a, cus, stream);
+        case 3: return launch_dm<3>(a, cus, stream);
+        case 4: return launch_dm<4>(a, cus, stream);
+        case 5: return launch_dm<5>(a, cus, stream);
+        case 6: return launch_dm<6>(a, cus, stream);
+        case 7: return launch_dm<7>(a, cus, stream);
+        case 8: return launch_dm<8>(a, cus, stream);
         default: return hipErrorInvalidValue;
     }
 }

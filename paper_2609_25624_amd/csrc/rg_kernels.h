@@ -68,7 +68,8 @@ hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, fl
 hipError_t launch_ktile(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
                         int bm, int bn, int nt, int reverse, hipStream_t stream);
 // Fixed-order decode attention (include/rg_attn.h).  The workspace regions are
-// carved by the caller: t [B][H][Lmax], segmax and spart [B][H][J], npart [B][H][J][D].
+// carved by the caller: t [B][H][Lmax], segmax and spart [B][H][J], mmax [B][H],
+// npart [B][H][J][D].  `cus`: compute units of the device (sizes the persistent grids).
 struct AttnArgs {
     const float* q;
     const uint16_t* k;
@@ -78,11 +79,13 @@ struct AttnArgs {
     float* t;
     float* segmax;
     float* spart;
+    float* mmax;
     float* npart;
     int64_t B, H, Hkv, Lmax, D, J;   // J = ceil(Lmax / 256)
     float scale;
+    uint32_t vmagic;                 // ceil(2^32 / (D / 8)) for D / 8 > 1 (row of a 16-byte vector)
 };
-hipError_t launch_attn(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn(const AttnArgs& a, int cus, hipStream_t stream);
 
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream);
 hipError_t launch_argmax(const float* y, int64_t* out, int64_t M, int64_t N, hipStream_t stream);
