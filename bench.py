@@ -155,6 +155,7 @@ def run_configs():
         del xd, ws, w0, y
         torch.cuda.empty_cache()
     run_variant_configs()
+    run_attention_configs()
 
 
 # The NEXT-row variants, timed the same way: FP32 weights (rg_linear_f32w; weight
@@ -220,6 +221,68 @@ def run_variant_configs():
             "bitexact": exact, "checked": "all", "kernel": plan["kernel_name"], "grid_wgs": plan["grid_wgs"],
             "rotated_copies": nrot}), flush=True)
         del xd, ws, w0, y
+        torch.cuda.empty_cache()
+
+
+# The fixed-order decode attention (rg_attn_decode), timed the same way: KV-cache
+# bytes (keys and values, bf16) per call over the call time.
+ATTN_CONFIGS = [  # (name, B, H, Hkv, Lmax, D)
+    ("llama3_8b_b16_l4096", 16, 32, 8, 4096, 128),
+    ("llama3_8b_b64_l2048", 64, 32, 8, 2048, 128),
+    ("llama3_8b_b1_l32768", 1, 32, 8, 32768, 128),
+    ("llama3_70b_b32_l4096", 32, 64, 8, 4096, 128),
+]
+
+
+def run_attention_configs():
+    import numpy as np
+    import torch
+
+    import oracle
+    import synth
+    import paper_2609_25624_amd as rg
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    for name, B, H, Hkv, Lmax, D in ATTN_CONFIGS:
+        q, kc, vc = synth.attn_inputs(B, H, Hkv, Lmax, D, seed=0)
+        lens = np.full(B, Lmax, dtype=np.int32)
+        kvb = 2 * kc.nbytes
+        nrot = max(1, int(np.ceil(ROTATE_BYTES / kvb)))
+        qd = torch.from_numpy(q).to(dev)
+        kds = [torch.from_numpy(kc.view(np.int16)).to(dev)]
+        vds = [torch.from_numpy(vc.view(np.int16)).to(dev)]
+        kds += [kds[0].clone() for _ in range(nrot - 1)]
+        vds += [vds[0].clone() for _ in range(nrot - 1)]
+        ld = torch.from_numpy(lens).to(dev)
+        out = torch.empty_like(qd)
+        ws = torch.empty(rg.rg_attn_workspace_size(B, H, Lmax, D), dtype=torch.uint8, device=dev)
+        scale = np.float32(1.0 / np.sqrt(D))
+        call = lambda i: rg.rg_attn_decode(qd, kds[i % nrot], vds[i % nrot], ld, out, scale, workspace=ws,
+                                           stream=stream)
+        for i in range(5):
+            call(i)
+        loops = []
+        for rep in range(5):
+            a = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for i in range(50):
+                call(i)
+            e.record(stream)
+            torch.cuda.synchronize()
+            loops.append(a.elapsed_time(e) * 1e3 / 50)
+        us = sorted(loops)[2]
+        call(0)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        want = oracle.attn_decode(q, kc, vc, lens, scale)
+        exact = bool(np.array_equal(got.view(np.uint32), want.view(np.uint32)))
+        print(json.dumps({
+            "variant": "attention", "config": name, "B": B, "H": H, "Hkv": Hkv, "L": Lmax, "D": D,
+            "us_per_call": round(us, 3), "kv_bytes": int(kvb), "kv_TBs": round(kvb / (us * 1e-6) / 1e12, 4),
+            "frac_of_8TBs": round(kvb / (us * 1e-6) / (HBM_PEAK_GBS * 1e9), 4), "bitexact": exact,
+            "checked": "all", "rotated_copies": nrot}), flush=True)
+        del kds, vds, ws, qd
         torch.cuda.empty_cache()
 
 
