@@ -42,9 +42,14 @@ def parse():
     ap.add_argument("--configs", action="store_true",
                     help="instead of the one-line step benchmark, time every config (M=1 8B layers, M=4/16/64, "
                          "LM head M=1/16, 70B layers at M=1 and M=2048) and print one JSON line each")
+    ap.add_argument("--attention", action="store_true",
+                    help="only the fixed-order decode attention configurations (one JSON line each)")
     ap.add_argument("--trace-summary", metavar="KERNEL_TRACE_CSV",
                     help="summarise a rocprofv3 --kernel-trace CSV of a run of this script made with the same "
                          "--steps/--warmup/--per-layer-calls (no GPU needed) and exit")
+    ap.add_argument("--attn-trace-summary", metavar="KERNEL_TRACE_CSV",
+                    help="summarise a rocprofv3 --kernel-trace CSV of 'bench.py --attention' per configuration "
+                         "(no GPU needed) and exit")
     ap.add_argument("--counter-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise the rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE CSVs of two --profile-kernels "
                          "runs into HBM bytes per gate+up launch (no GPU needed) and exit")
@@ -322,6 +327,27 @@ def trace_summary(path, args):
     print("\n".join(lines))
 
 
+def attn_trace_summary(path):
+    """Per-configuration kernel durations from a rocprofv3 kernel trace of 'bench.py --attention'.
+    Each configuration makes 5 + 5 * 50 + 1 calls of four kernels, in ATTN_CONFIGS order."""
+    rows = [r for r in _csv_rows(path) if "attn_" in r["Kernel_Name"]]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    per = 4 * (5 + 5 * 50 + 1)
+    print(f"dispatches of the attention kernels: {len(rows)}")
+    print(f"{'config':22s} {'scores_us':>10s} {'max_us':>8s} {'partials_us':>12s} {'fold_us':>8s} {'sum_us':>8s} {'KV TB/s':>8s}")
+    for c, (name, B, H, Hkv, Lmax, D) in enumerate(ATTN_CONFIGS):
+        blk = rows[c * per:(c + 1) * per][4 * 5:4 * (5 + 5 * 50)]       # the timed calls
+        avg = {}
+        for key in ("scores", "max", "partials", "fold"):
+            d = [dur(r) for r in blk if f"attn_{key}_kernel" in r["Kernel_Name"]]
+            avg[key] = sum(d) / len(d)
+        tot = sum(avg.values())
+        kvb = 2 * B * Hkv * Lmax * D * 2
+        print(f"{name:22s} {avg['scores']:10.2f} {avg['max']:8.2f} {avg['partials']:12.2f} {avg['fold']:8.2f} "
+              f"{tot:8.2f} {kvb / (tot * 1e-6) / 1e12:8.3f}")
+
+
 def counter_summary(fetch_csv, write_csv):
     """HBM bytes per gate+up launch from FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each scaled by the
     reading of the same counter for a 256 MiB device-to-device copy (reads and writes 256 MiB)."""
@@ -374,6 +400,9 @@ def main():
     if args.trace_summary:
         trace_summary(args.trace_summary, args)
         return
+    if args.attn_trace_summary:
+        attn_trace_summary(args.attn_trace_summary)
+        return
     if args.counter_summary:
         counter_summary(*args.counter_summary)
         return
@@ -398,6 +427,9 @@ def main():
         return
     if args.configs:
         run_configs()
+        return
+    if args.attention:
+        run_attention_configs()
         return
     stream = torch.cuda.current_stream()
 
