@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--counter-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise the rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE CSVs of two --profile-kernels "
                          "runs into HBM bytes per gate+up launch (no GPU needed) and exit")
+    ap.add_argument("--inst-summary", metavar="COUNTER_CSV",
+                    help="summarise a rocprofv3 --pmc SQ_INSTS_VALU_FMA_F32 SQ_INSTS_MFMA SQ_INSTS_VALU_ADD_F32 "
+                         "SQ_INSTS_VALU run of --profile-kernels (no GPU needed) and exit")
     ap.add_argument("--profile-kernels", action="store_true",
                     help="short run for hardware counters: 20 launches of the gate+up M=1 layer, then 5 plain "
                          "device copies of 256 MiB (the calibration kernel for HBM byte counters)")
@@ -348,6 +351,19 @@ def attn_trace_summary(path):
               f"{tot:8.2f} {kvb / (tot * 1e-6) / 1e12:8.3f}")
 
 
+def inst_summary(path):
+    """Instruction counts per gate+up launch: every FMA is one full-wave binary32 FMA per weight
+    (N*K/64 wave instructions at M = 1) and no matrix-core instruction is issued."""
+    N, K = 28672, 4096
+    rows = [r for r in _csv_rows(path) if "rg::" in r["Kernel_Name"]]
+    names = sorted({r["Counter_Name"] for r in rows})
+    for c in names:
+        v = [float(r["Counter_Value"]) for r in rows if r["Counter_Name"] == c]
+        print(f"{c}: {sum(v) / len(v):.0f} per launch over {len(v)} launches")
+    print(f"expected SQ_INSTS_VALU_FMA_F32 = N*K/64 = {N * K // 64}; expected SQ_INSTS_MFMA = 0")
+    print(f"kernel_source_hash = {_kernel_hash()}")
+
+
 def counter_summary(fetch_csv, write_csv):
     """HBM bytes per gate+up launch from FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each scaled by the
     reading of the same counter for a 256 MiB device-to-device copy (reads and writes 256 MiB)."""
@@ -399,6 +415,9 @@ def main():
     args = parse()
     if args.trace_summary:
         trace_summary(args.trace_summary, args)
+        return
+    if args.inst_summary:
+        inst_summary(args.inst_summary)
         return
     if args.attn_trace_summary:
         attn_trace_summary(args.attn_trace_summary)
