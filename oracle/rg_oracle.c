@@ -8,10 +8,10 @@
  * in ONE fixed floating-point order, written out literally:
  *
  *   up(b)  = the float whose bits are (uint32)b << 16        (exact widening
- *            of a bfloat16 pattern done "in registers", Design, eq. 2)
+ *            of a bfloat16 pattern, done in registers: Design, eq. 2)
  *   C      = 256,  J = ceil(K / C)                          (segments are a
- *            pure function of K, rule R3; the segment length is this build's
- *            reading, the paper never prints its pinned value)
+ *            pure function of K, rule R3; the segment length is a reading,
+ *            the paper never prints its pinned value)
  *   p_j    = +0.0f, then for k = jC .. min(jC+C, K)-1 ascending:
  *               p_j = fmaf(x[m,k], up(W[n,k]), p_j)         (IEEE-754 FMA only,
  *            rule R1; each segment accumulated sequentially in ascending k,

@@ -15,7 +15,7 @@ def pytest_configure(config):
 
 def pytest_collection_modifyitems(config, items):
     # GPU tests only make sense when a device is present; on a CPU-only host they are skipped
-    # rather than failed (the driver selects them with -m gpu on the GPU machine).
+    # rather than failed (they are selected with -m gpu where the GPU is).
     try:
         import torch
         have_gpu = torch.cuda.is_available()
