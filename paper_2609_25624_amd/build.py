@@ -23,10 +23,30 @@ NEGCTL_LIB = os.path.join(HERE, "librg_negctl.so")
 NEGCTL_SOURCES = ["rg_negctl.hip"]
 
 
+# A C program that uses the library through include/rg.h only (no Python).
+EXAMPLE_SRC = os.path.join(HERE, "examples", "linear_capi.c")
+EXAMPLE_BIN = os.path.join(HERE, "examples", "linear_capi")
+
+
 def build(verbose: bool = False) -> str:
     _build_lib(SOURCES, LIB, verbose)
     _build_lib(NEGCTL_SOURCES, NEGCTL_LIB, verbose)
+    _build_example(verbose)
     return LIB
+
+
+def _build_example(verbose):
+    # host-only C99, built by the system C compiler: the C-ABI needs no HIP compiler on the caller's side
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(HIPCC)))
+    cmd = ["gcc", "-std=c99", "-O2", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(rocm, "include"),
+           EXAMPLE_SRC, "-L" + HERE, "-lrg", "-L" + os.path.join(rocm, "lib"), "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN/..", "-Wl,-rpath," + os.path.join(rocm, "lib"), "-o", EXAMPLE_BIN + ".tmp"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("example build failed:\n" + r.stderr)
+    os.replace(EXAMPLE_BIN + ".tmp", EXAMPLE_BIN)
 
 
 def _build_lib(sources, lib, verbose):
