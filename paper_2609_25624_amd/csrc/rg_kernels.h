@@ -23,6 +23,7 @@ struct DecodeArgs {
     int groups;         // row groups (workgroups per slice)
     int mslices;        // slices of MT rows of x (decode_kernel only; 1 otherwise)
     int max_rows_wg;    // 4 * ceil(Q / grid): rows staged per workgroup
+    int round_major;    // 1: quads placed round-major over the grid, 0: one contiguous range each
 };
 
 // Arguments of the M == 1 dense-stream kernel (K % 256 == 0, K >= 4096).

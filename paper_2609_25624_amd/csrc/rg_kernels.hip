@@ -190,13 +190,67 @@ __global__ void __launch_bounds__(256) generic_kernel(const float* __restrict__ 
     }
 }
 
+// First quad of each round of a workgroup in the decode kernels.  The Q quads
+// are split over G workgroups as evenly as possible (qb = Q / G each, one more
+// for the first qr = Q % G) and taken RQ at a time.  Contiguous placement:
+// each workgroup owns one range of quads.  Round-major placement: the quads
+// all workgroups take in round r form one contiguous window [T(r), T(r+1)),
+// in workgroup order, where T(r) counts the quads taken in the rounds before
+// r, so at any moment the grid streams neighbouring rows of W rather than G
+// ranges far apart (measured faster for one or two rows of x, slower for four).
+// In round-major placement every round before r_full = qb / RQ is full for
+// every workgroup (round r starts at (r G + g) RQ), and a workgroup has at
+// most r_full + 1 rounds, so only round r_full needs the general count.
+template <bool RM>
+struct QuadPlace {
+    int64_t base, step;   // rounds r < r_full start at base + r * step (every round when !RM)
+    int r_full;
+    int64_t last;         // first quad of round r_full (RM)
+    __device__ int64_t start(int r) const {
+        if constexpr (!RM) return base + (int64_t)r * step;
+        else return r < r_full ? base + (int64_t)r * step : last;
+    }
+};
+
+template <bool RM>
+__device__ __forceinline__ QuadPlace<RM> quad_place(int g, int G, int64_t qb, int qr, int RQ) {
+    QuadPlace<RM> p;
+    if constexpr (!RM) {
+        p.base = (int64_t)g * qb + min(g, qr);
+        p.step = RQ;
+        p.r_full = 0;
+        p.last = 0;
+    } else {
+        p.base = (int64_t)g * RQ;
+        p.step = (int64_t)G * RQ;
+        p.r_full = (int)(qb / RQ);
+        const int64_t done = (int64_t)p.r_full * RQ;                          // quads a workgroup took before
+        const int64_t c1 = min((int64_t)RQ, max((int64_t)0, qb + 1 - done));  // taken in round r_full by g < qr
+        const int64_t c0 = min((int64_t)RQ, max((int64_t)0, qb - done));      // ... and by the others
+        const int64_t before = (int64_t)qr * min(qb + 1, done) + (int64_t)(G - qr) * min(qb, done);
+        p.last = before + (int64_t)min(g, qr) * c1 + (int64_t)max(0, g - qr) * c0;
+    }
+    return p;
+}
+
+// Global row of staged result row o (rows of the workgroup in round order).
+template <bool RM>
+__device__ __forceinline__ int64_t staged_row(const QuadPlace<RM>& p, int o, int RQ) {
+    if constexpr (!RM) return 4 * p.base + o;   // one contiguous range
+    else {
+        const int r = o / (4 * RQ);
+        return 4 * p.start(r) + (o - 4 * RQ * r);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // decode kernel (M <= MT <= 4): streaming GEMV / skinny GEMM.
 //
-// Work split.  Rows of W are grouped in quads (4 rows).  Workgroup g owns the
-// contiguous quads [q0, q1) and all of K for them, so every output is
+// Work split.  Rows of W are grouped in quads (4 rows).  Workgroup g owns a
+// balanced share of the quads and all of K for them, so every output is
 // finished inside one workgroup (no cross-workgroup traffic, no atomics).
-// It walks its quads in rounds of RQ quads.  In a round every lane owns one
+// It walks its quads in rounds of RQ quads, placed contiguously or
+// round-major over the grid (quad_place).  In a round every lane owns one
 // (row, segment) pair: the 4 lanes of a DPP quad hold 4 consecutive rows and
 // one segment j; the lane roles (quad-in-round, j, row-in-quad) are fixed for
 // the whole kernel, so each lane keeps x of its segment in registers.
@@ -284,7 +338,7 @@ __device__ __forceinline__ void fma_slab(const uint4 (&wp)[8], const float (&X)[
 constexpr int kSlab = 64;                    // elements per lane per step
 constexpr int kSlabBytesPerWave = 64 * 128;  // 8 KB
 
-template <int MT, int NW, int DEPTH>
+template <int MT, int NW, int DEPTH, bool RM>
 __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     static_assert(MT == 1 || MT == 2 || MT == 4, "decode M tile");
     static_assert(DEPTH >= 2 && DEPTH <= 3, "pipeline depth");
@@ -317,8 +371,8 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     float* yg = a.y + (int64_t)slice * MT * N;
     const int64_t Ms = a.M - (int64_t)slice * MT;           // rows of x in this slice (>= 1)
     // balanced split of the Q quads over the row groups (the first qrem take one more)
-    const int64_t q0 = (int64_t)g * a.qbase + min(g, a.qrem);
     const int nq = (int)a.qbase + (g < a.qrem ? 1 : 0);
+    const QuadPlace<RM> place = quad_place<RM>(g, a.groups, a.qbase, a.qrem, RQ);
     const int rounds = (nq + RQ - 1) / RQ;
     const int nsteps = rounds * (kChunk / kSlab);
 
@@ -388,7 +442,7 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     // Issue step st (round r = st/4, slab s = st%4) into ring slot st % DEPTH.
     auto issue = [&](int st) {
         const int r = st >> 2, s = st & 3;
-        const int64_t row0 = 4 * (q0 + (int64_t)r * RQ);     // first row of the round
+        const int64_t row0 = 4 * place.start(r);              // first row of the round
         const int64_t rmax = N - 1 - row0;                    // clamp rows to W
         const char* base = reinterpret_cast<const char*>(a.w) + row0 * row_bytes;
         const uint32_t slot = ring_base + (uint32_t)((st % DEPTH) * kSlabBytesPerWave);
@@ -468,10 +522,9 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
     vmcnt_wait<0>();
     __syncthreads();
     // ---- write results ----
-    const int64_t rowbase = 4 * q0;
     for (int o = tid; o < rows_wg * MT; o += kThreads) {
         const int m = o / rows_wg, rl = o % rows_wg;
-        const int64_t n = rowbase + rl;
+        const int64_t n = staged_row(place, rl, RQ);
         if (m < Ms && n < N) {
             const float v = yres[rl * MT + m];
             yg[(int64_t)m * N + n] = a.bias ? v + a.bias[n] : v;
@@ -536,7 +589,7 @@ __device__ __forceinline__ void fma_slab1(const uint4 (&wp)[8], const float (&Xs
     }
 }
 
-template <int NW, int DEPTH>
+template <int NW, int DEPTH, bool RM>
 __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
     static_assert(DEPTH >= 2 && DEPTH <= 3, "pipeline depth");
     constexpr int kThreads = NW * 64;
@@ -554,12 +607,14 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
     const int RQ = a.RQ;
     const int64_t N = a.N, K = a.K;
 
-    // balanced split of the Q quads over the grid (the first qrem workgroups take one more)
-    const int g = a.reverse ? (int)(gridDim.x - 1 - blockIdx.x) : (int)blockIdx.x;
-    const int64_t q0 = (int64_t)g * a.qbase + min(g, a.qrem);
+    // balanced split of the Q quads over the grid (the first qrem workgroups take one more),
+    // placed as quad_place says
+    const int G = (int)gridDim.x;
+    const int g = a.reverse ? G - 1 - (int)blockIdx.x : (int)blockIdx.x;
     const int nq = (int)a.qbase + (g < a.qrem ? 1 : 0);
     const int rounds = (nq + RQ - 1) / RQ;
     const int nsteps = rounds * (kChunk / kSlab);
+    const QuadPlace<RM> place = quad_place<RM>(g, G, a.qbase, a.qrem, RQ);
 
     // ---- fixed lane role (consumer) ----
     const int ql = tid >> 2;
@@ -627,7 +682,7 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
 
     auto issue = [&](int st) {
         const int r = st >> 2, s = st & 3;
-        const int64_t row0 = 4 * (q0 + (int64_t)r * RQ);
+        const int64_t row0 = 4 * place.start(r);
         const int64_t rmax = N - 1 - row0;
         const char* base = reinterpret_cast<const char*>(a.w) + row0 * row_bytes;
         const uint32_t slot = ring_base + (uint32_t)((st % DEPTH) * kSlabBytesPerWave);
@@ -699,9 +754,8 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
     }
     vmcnt_wait<0>();
     __syncthreads();
-    const int64_t rowbase = 4 * q0;
     for (int o = tid; o < rows_wg; o += kThreads) {
-        const int64_t n = rowbase + o;
+        const int64_t n = staged_row(place, o, RQ);
         if (n < N) a.y[n] = a.bias ? yres[o] + a.bias[n] : yres[o];
     }
 }
@@ -1471,10 +1525,19 @@ hipError_t launch_generic(const float* x, const float* w, const float* bias, flo
     return launch_generic_t(x, w, bias, y, M, N, K, grid, reverse, stream);
 }
 
+// Round-major placement is built for MT <= 2 only (the host never asks for it with 4 rows).
 template <int MT, int NW, int DEPTH>
 static hipError_t launch_decode_t(const DecodeArgs& a, int grid, hipStream_t stream) {
     const size_t dyn = (size_t)a.max_rows_wg * MT * sizeof(float);
-    hipLaunchKernelGGL((decode_kernel<MT, NW, DEPTH>), dim3(grid), dim3(NW * 64), dyn, stream, a);
+    if constexpr (MT <= 2) {
+        if (a.round_major) {
+            hipLaunchKernelGGL((decode_kernel<MT, NW, DEPTH, true>), dim3(grid), dim3(NW * 64), dyn, stream, a);
+            return hipGetLastError();
+        }
+    } else {
+        if (a.round_major) return hipErrorInvalidValue;
+    }
+    hipLaunchKernelGGL((decode_kernel<MT, NW, DEPTH, false>), dim3(grid), dim3(NW * 64), dyn, stream, a);
     return hipGetLastError();
 }
 
@@ -1510,7 +1573,8 @@ static hipError_t launch_decode_w(const DecodeArgs& a, int grid, int nw, int dep
 template <int NW, int DEPTH>
 static hipError_t launch_decode1_t(const DecodeArgs& a, int grid, hipStream_t stream) {
     const size_t dyn = (size_t)a.max_rows_wg * sizeof(float);
-    hipLaunchKernelGGL((decode1_kernel<NW, DEPTH>), dim3(grid), dim3(NW * 64), dyn, stream, a);
+    if (a.round_major) hipLaunchKernelGGL((decode1_kernel<NW, DEPTH, true>), dim3(grid), dim3(NW * 64), dyn, stream, a);
+    else hipLaunchKernelGGL((decode1_kernel<NW, DEPTH, false>), dim3(grid), dim3(NW * 64), dyn, stream, a);
     return hipGetLastError();
 }
 

@@ -196,6 +196,26 @@ def test_gemv_shapes(N, K):
         rg.rg_linear_set_launch(None)
 
 
+@pytest.mark.parametrize("M,kernel", [(1, "decode_xs"), (1, "decode"), (2, "decode")])
+@pytest.mark.parametrize("N,K", [(1030, 4096), (4097, 1000), (515, 14336), (6141, 4352)])
+@pytest.mark.parametrize("grid,order", [(3, 0), (7, 1), (13, 0)])
+def test_round_major_quad_placement(M, kernel, N, K, grid, order):
+    """The streaming decode kernels with four or more rounds per workgroup (quads placed
+    round-major over the grid for one or two rows of x): even and uneven splits (Q % grid),
+    a short last round, a last quad with fewer than 4 rows, reversed workgroup order."""
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(kernel=kernel, grid_wgs=grid, grid_order=order)
+    try:
+        p = rg.rg_plan(M, N, K)
+        assert p["kernel_name"] == kernel
+        Q = -(-N // 4)
+        rounds = -(-(-(-Q // p["grid_wgs"])) // (p["rows_per_round"] // 4))
+        assert rounds >= 4, rounds
+        _check_layer(M, N, K, seed=M * 31 + N + K + grid)
+    finally:
+        rg.rg_linear_set_launch(None)
+
+
 @pytest.mark.parametrize("M", [2, 5, 9, 16, 17, 33, 64, 100])
 @pytest.mark.parametrize("N,K", [(3, 4096), (1030, 4104), (301, 8192), (130, 14336), (77, 520)])
 @pytest.mark.parametrize("tile_n,waves", [(0, 0), (16, 4), (16, 8), (32, 0), (64, 0)])
