@@ -264,7 +264,14 @@ bool attn_layout(int64_t B, int64_t H, int64_t Lmax, int64_t D, AttnLayout* lay)
 }
 
 // Register-tiled kernel: the largest tile that still gives every CU a few workgroups.
-int tiled_schedule(int64_t M, int64_t N, Plan* p) {
+// Register tiles for large M.  The 128 x 128 tile has two builds (waves per
+// SIMD, reported in `depth`).  Per round of resident workgroups (2 or 3 per
+// CU) the three-wave build is no faster than the two-wave one (its spills cost
+// what the third wave gains: 7168 tiles 82 against 84 TFLOP/s, 1024 tiles 69
+// against 86), so it is taken only where it fills its rounds clearly better:
+// 639 tiles fill 0.62 of two rounds of 512 but 0.83 of one round of 768
+// (64 against 59 TFLOP/s).
+int tiled_schedule(int64_t M, int64_t N, const rg_launch_t& o, Plan* p) {
     const int64_t t128 = ceil_div(M, 128) * ceil_div(N, 128);
     const int64_t t64x128 = ceil_div(M, 64) * ceil_div(N, 128);
     if (t128 >= 2 * kNominalCUs) { p->tile_m = 128; p->tile_n = 128; }
@@ -274,6 +281,14 @@ int tiled_schedule(int64_t M, int64_t N, Plan* p) {
     if (tiles > 0x7fffffff) return RG_ERR_RANGE;
     p->grid = (int)tiles;
     p->nw = 4;
+    p->depth = 0;
+    if (p->tile_m == 128) {
+        const double s2 = 2.0 * kNominalCUs, s3 = 3.0 * kNominalCUs;
+        const double fill2 = (double)tiles / (ceil_div(tiles, (int64_t)s2) * s2);
+        const double fill3 = (double)tiles / (ceil_div(tiles, (int64_t)s3) * s3);
+        p->depth = (tiles > (int64_t)s2 && fill3 >= 1.2 * fill2) ? 3 : 2;
+        if (o.depth > 0) p->depth = o.depth;
+    }
     return RG_OK;
 }
 
@@ -349,7 +364,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
             p->mslices = 1;
         }
     }
-    if (p->kernel == RG_KERNEL_TILED) return tiled_schedule(M, N, p);
+    if (p->kernel == RG_KERNEL_TILED) return tiled_schedule(M, N, o, p);
     if (p->kernel == RG_KERNEL_GENERIC) generic_schedule(M, N, o, p);
     return RG_OK;
 }
@@ -375,7 +390,7 @@ int make_plan_f32w(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launc
     p->mslices = 1;
     if (want == RG_KERNEL_STREAM) return stream_schedule(M, N, o, p) ? RG_OK : RG_ERR_RANGE;
     if (want == RG_KERNEL_KTILE) return ktile_schedule(M, N, K, o, p) ? RG_OK : RG_ERR_RANGE;
-    if (want == RG_KERNEL_TILED) return tiled_schedule(M, N, p);
+    if (want == RG_KERNEL_TILED) return tiled_schedule(M, N, o, p);
     generic_schedule(M, N, o, p);
     return RG_OK;
 }
@@ -549,7 +564,7 @@ int linear_impl(const float* x, const uint16_t* w, const float* bias, float* y, 
     } else if (p.kernel == RG_KERNEL_KTILE) {
         e = rg::launch_ktile(x, w, bias, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.reverse, st);
     } else if (p.kernel == RG_KERNEL_TILED) {
-        e = rg::launch_tiled(x, w, bias, y, M, N, K, p.tile_m, p.tile_n, p.reverse, st);
+        e = rg::launch_tiled(x, w, bias, y, M, N, K, p.tile_m, p.tile_n, p.depth, p.reverse, st);
     } else {
         e = rg::launch_generic(x, w, bias, y, M, N, K, p.grid, p.reverse, st);
     }
@@ -577,7 +592,7 @@ int linear_f32w_impl(const float* x, const float* w, float* y, int64_t M, int64_
     } else if (p.kernel == RG_KERNEL_KTILE) {
         e = rg::launch_ktile(x, w, nullptr, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.reverse, st);
     } else if (p.kernel == RG_KERNEL_TILED) {
-        e = rg::launch_tiled(x, w, nullptr, y, M, N, K, p.tile_m, p.tile_n, p.reverse, st);
+        e = rg::launch_tiled(x, w, nullptr, y, M, N, K, p.tile_m, p.tile_n, p.depth, p.reverse, st);
     } else {
         e = rg::launch_generic(x, w, nullptr, y, M, N, K, p.grid, p.reverse, st);
     }

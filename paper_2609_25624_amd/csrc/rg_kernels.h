@@ -60,10 +60,11 @@ hipError_t launch_stream(const StreamArgs& a, bool f32_weights, int mt, int grid
 hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipStream_t stream);
 hipError_t launch_gemv(const GemvArgs& a, int grid, int nw, hipStream_t stream);
+// occ: waves per SIMD of the 128 x 128 tile build (2 or 3; ignored by the other tiles)
 hipError_t launch_tiled(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int reverse, hipStream_t stream);
+                        int bm, int bn, int occ, int reverse, hipStream_t stream);
 hipError_t launch_tiled(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int reverse, hipStream_t stream);
+                        int bm, int bn, int occ, int reverse, hipStream_t stream);
 hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
                         int bm, int bn, int nt, int reverse, hipStream_t stream);
 hipError_t launch_ktile(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,

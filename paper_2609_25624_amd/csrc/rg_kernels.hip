@@ -772,6 +772,19 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
 // output keeps two registers: the running chain of the current 256-wide
 // segment (from +0, ascending k) and the fold of the finished segments
 // (first segment taken as is, later ones added in ascending order).
+//
+// Every slab runs all 16 steps: the missing k of a short last slab are
+// staged as +0 in x and W, and fmaf(+0, +0, p) = p for a chain that started
+// at +0 (such a chain is never -0), so the padded steps change no bit.
+//
+// Occupancy.  One wave issues a VALU instruction only every few cycles on
+// gfx950 (measured with independent FMAs: ~51 TFLOP/s at one wave per SIMD,
+// ~96 at two, ~125 at four), so the 128 x 128 tile comes in two builds:
+// two waves per SIMD with the next step's operands read ahead (204 registers,
+// no spills), and three waves per SIMD (at most 168 registers: one operand
+// set per step, a few registers spilled outside the FMA loop).  Per round of
+// resident workgroups the two are about equally fast; the planner takes the
+// three-wave build where its rounds of 3 workgroups per CU are clearly fuller.
 // ---------------------------------------------------------------------------
 constexpr int kTK = 16;   // k per slab
 
@@ -791,10 +804,11 @@ __device__ __forceinline__ void lds_vec(const float* p, float* out) {
     }
 }
 
-template <int BM, int BN, typename WT>
-__global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x, const WT* __restrict__ w,
-                                                    const float* __restrict__ bias, float* __restrict__ y, int64_t M, int64_t N, int64_t K,
-                                                    int reverse) {
+// W3: the three-waves-per-SIMD build (one operand set per step).
+template <int BM, int BN, typename WT, bool W3>
+__device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT* __restrict__ w,
+                                           const float* __restrict__ bias, float* __restrict__ y, int64_t M,
+                                           int64_t N, int64_t K, int reverse) {
     constexpr int TM = BM / 16, TN = BN / 16;        // per-thread outputs per dimension
     constexpr int HM = TM / 2, HN = TN / 2;          // two interleaved halves
     static_assert(TM % 2 == 0 && TN % 2 == 0, "tile");
@@ -808,7 +822,8 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
     const int64_t b = reverse ? (int64_t)(gridDim.x - 1 - blockIdx.x) : (int64_t)blockIdx.x;
     const int64_t m0 = (b / tiles_n) * BM, n0 = (b % tiles_n) * BN;
 
-    // staging roles: x tile BM x 16 floats, W tile BN x 16 weights (16-byte vectors of WE)
+    // staging roles: x tile BM x 16 floats, W tile BN x 16 weights (16-byte vectors of WE);
+    // k >= K is staged as +0 (K % 8 == 0 on this path, so a vector is wholly in or out)
     using WV = WVec<WT>;
     constexpr int WE = WV::E, WPR = kTK / WE;        // weights per vector, vectors per tile row
     constexpr int XF4 = BM * kTK / 4 / 256;          // float4 loads per thread for x
@@ -868,8 +883,9 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
     for (int64_t sl = 0; sl < nslabs; ++sl) {
         const int buf = (int)(sl & 1);
         if (sl + 1 < nslabs) load_slab((sl + 1) * kTK);
-        const int kvalid = (int)min((int64_t)kTK, K - sl * kTK);
-        if (kvalid == kTK) {
+        if constexpr (W3) {
+            // one operand set per step; the scheduling barrier keeps later steps' reads from
+            // being hoisted into registers (three waves per SIMD hide the LDS latency instead)
 #pragma unroll
             for (int kk = 0; kk < kTK; ++kk) {
                 float xv[TM], wv[TN];
@@ -882,25 +898,31 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_fmaf(xv[i], wv[j], acc[i][j]);
+                __builtin_amdgcn_sched_barrier(0);
             }
         } else {
-            for (int kk = 0; kk < kvalid; ++kk) {
-                float xv[TM], wv[TN];
+            // operands of step kk + 1 are read from LDS while step kk's FMAs run
+            float xv[2][TM], wv[2][TN];
+            auto read_k = [&](int kk, int r) {
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
-#pragma unroll
-                    for (int q = 0; q < HM; ++q) xv[h * HM + q] = xs[buf][kk][h * (BM / 2) + tm * HM + q];
-#pragma unroll
-                    for (int q = 0; q < HN; ++q) wv[h * HN + q] = ws[buf][kk][h * (BN / 2) + tn * HN + q];
+                    lds_vec<HM>(&xs[buf][kk][h * (BM / 2) + tm * HM], &xv[r][h * HM]);
+                    lds_vec<HN>(&ws[buf][kk][h * (BN / 2) + tn * HN], &wv[r][h * HN]);
                 }
+            };
+            read_k(0, 0);
+#pragma unroll
+            for (int kk = 0; kk < kTK; ++kk) {
+                const int r = kk & 1;
+                if (kk + 1 < kTK) read_k(kk + 1, r ^ 1);
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
-                    for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_fmaf(xv[i], wv[j], acc[i][j]);
+                    for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_fmaf(xv[r][i], wv[r][j], acc[i][j]);
             }
         }
         // end of a 256-wide segment (or of K): fold the segment chain, restart it from +0
-        const int64_t kend = sl * kTK + kvalid;
+        const int64_t kend = min((sl + 1) * kTK, K);
         if ((kend % kChunk) == 0 || kend == K) {
             const bool first = kend <= kChunk;
 #pragma unroll
@@ -926,6 +948,21 @@ __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x,
             if (gn < N) y[gm * N + gn] = bias ? tot[i][j] + bias[gn] : tot[i][j];
         }
     }
+}
+
+template <int BM, int BN, typename WT>
+__global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x, const WT* __restrict__ w,
+                                                    const float* __restrict__ bias, float* __restrict__ y, int64_t M,
+                                                    int64_t N, int64_t K, int reverse) {
+    tiled_body<BM, BN, WT, false>(x, w, bias, y, M, N, K, reverse);
+}
+
+// The 128 x 128 tile built for three waves per SIMD.
+template <typename WT>
+__global__ void __launch_bounds__(256, 3) tiled3_kernel(const float* __restrict__ x, const WT* __restrict__ w,
+                                                       const float* __restrict__ bias, float* __restrict__ y,
+                                                       int64_t M, int64_t N, int64_t K, int reverse) {
+    tiled_body<128, 128, WT, true>(x, w, bias, y, M, N, K, reverse);
 }
 
 // ---------------------------------------------------------------------------
@@ -1628,11 +1665,12 @@ hipError_t launch_decode(const DecodeArgs& a, int mt, int grid, int nw, int dept
 
 template <typename WT>
 static hipError_t launch_tiled_t(const float* x, const WT* w, const float* bias, float* y, int64_t M, int64_t N,
-                                 int64_t K, int bm, int bn, int reverse, hipStream_t stream) {
+                                 int64_t K, int bm, int bn, int occ, int reverse, hipStream_t stream) {
     const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid((unsigned)tiles), block(256);
-    if (bm == 128 && bn == 128) hipLaunchKernelGGL((tiled_kernel<128, 128, WT>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
+    if (bm == 128 && bn == 128 && occ == 3) hipLaunchKernelGGL((tiled3_kernel<WT>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
+    else if (bm == 128 && bn == 128 && occ == 2) hipLaunchKernelGGL((tiled_kernel<128, 128, WT>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
     else if (bm == 64 && bn == 128) hipLaunchKernelGGL((tiled_kernel<64, 128, WT>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
     else if (bm == 64 && bn == 64) hipLaunchKernelGGL((tiled_kernel<64, 64, WT>), grid, block, 0, stream, x, w, bias, y, M, N, K, reverse);
     else return hipErrorInvalidValue;
@@ -1640,13 +1678,13 @@ static hipError_t launch_tiled_t(const float* x, const WT* w, const float* bias,
 }
 
 hipError_t launch_tiled(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int reverse, hipStream_t stream) {
-    return launch_tiled_t(x, w, bias, y, M, N, K, bm, bn, reverse, stream);
+                        int bm, int bn, int occ, int reverse, hipStream_t stream) {
+    return launch_tiled_t(x, w, bias, y, M, N, K, bm, bn, occ, reverse, stream);
 }
 
 hipError_t launch_tiled(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int reverse, hipStream_t stream) {
-    return launch_tiled_t(x, w, bias, y, M, N, K, bm, bn, reverse, stream);
+                        int bm, int bn, int occ, int reverse, hipStream_t stream) {
+    return launch_tiled_t(x, w, bias, y, M, N, K, bm, bn, occ, reverse, stream);
 }
 
 // Small-M tiles (16 outputs per thread, K shared out over KS = 16 * nt / (bm * bn) groups).

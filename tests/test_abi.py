@@ -86,6 +86,24 @@ def test_gemv_schedule_defaults():
         rg.rg_linear_set_launch(None)
 
 
+def test_tiled_128_build_choice():
+    # three waves per SIMD only where its rounds of 768 resident tiles are clearly fuller than
+    # the two-wave build's rounds of 512; other tiles report depth 0
+    cases = {(2048, 8192, 8192): 2,     # 1024 tiles: 2 full rounds of 512, 1.33 rounds of 768
+             (2048, 57344, 8192): 2,    # 7168 tiles: 14 full rounds of 512
+             (2048, 4096, 4096): 2,     # 512 tiles: one round either way
+             (1100, 9000, 4096): 3}     # 639 tiles: 0.62 of two rounds of 512, 0.83 of one of 768
+    for shape, depth in cases.items():
+        p = rg.rg_plan(*shape)
+        assert (p["kernel_name"], p["tile_m"], p["depth"]) == ("tiled", 128, depth), (shape, p)
+    assert rg.rg_plan(256, 28672, 4096)["depth"] == 0          # 64 x 128 tiles
+    rg.rg_linear_set_launch(depth=3)
+    try:
+        assert rg.rg_plan(2048, 8192, 8192)["depth"] == 3
+    finally:
+        rg.rg_linear_set_launch(None)
+
+
 def test_set_launch_range_checks():
     for bad in (dict(waves_per_wg=9), dict(grid_wgs=-1), dict(depth=4), dict(depth=1), dict(grid_order=2), dict(kernel=8), dict(tile_n=48)):
         with pytest.raises(rg.RgError) as e:

@@ -175,6 +175,22 @@ def test_tiled_shapes(M, N, K):
     _check_layer(M, N, K, seed=M + K)
 
 
+@pytest.mark.parametrize("M,N,K", [(2048, 4100, 264), (2000, 4096, 1032), (4096, 2048, 520)])
+@pytest.mark.parametrize("depth,order", [(2, 0), (3, 0), (3, 1)])
+def test_tiled_128_builds(M, N, K, depth, order):
+    """The 128 x 128 prefill tile in both builds (two or three waves per SIMD), full outputs:
+    ragged M and N tiles, a short last segment, a short last slab (K % 16 = 8, staged as +0),
+    reversed workgroup order."""
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(kernel="tiled", depth=depth, grid_order=order)
+    try:
+        p = rg.rg_plan(M, N, K)
+        assert (p["kernel_name"], p["tile_m"], p["depth"]) == ("tiled", 128, depth)
+        _check_layer(M, N, K, seed=M + N + K + depth)
+    finally:
+        rg.rg_linear_set_launch(None)
+
+
 @pytest.mark.parametrize("M", [1, 2, 3, 4, 5, 9])
 @pytest.mark.parametrize("N,K", [(1, 8), (3, 16), (5, 248), (4, 256), (7, 264), (63, 1000), (65, 1016),
                                  (130, 4104), (33, 8200), (17, 520)])
