@@ -541,8 +541,11 @@ def main():
             grid_wgs=L["plan"]["grid_wgs"], rotated_copies=len(L["ws"]))
 
     # ---- bit-exactness of the last outputs against the CPU oracle ----
+    # (with the SHA-256 of each layer's output bytes: the inputs are fixed by their seeds, so
+    # the digest is the same on every run and every device that follows the order)
+    import hashlib
     import oracle
-    exact = {}
+    exact, digests = {}, {}
     for L in layers:
         rg.rg_linear(L["xd"], L["ws"][0], L["y"], stream=stream)
     torch.cuda.synchronize()
@@ -550,6 +553,7 @@ def main():
         want = oracle.linear(L["x"], L["w"])
         got = L["y"].cpu().numpy()
         exact[L["name"]] = bool(np.array_equal(got.view(np.uint32), want.view(np.uint32)))
+        digests[L["name"]] = hashlib.sha256(np.ascontiguousarray(got).tobytes()).hexdigest()[:16]
 
     # ---- roofline of the dominant kernel: the gate+up launch ----
     dom = next(L for L in layers if L["name"] == "gate_up")
@@ -631,6 +635,7 @@ def main():
                    "layers": {n: [N, K] for n, N, K in LAYERS}, "cold_weights": True},
         "bitexact_vs_oracle": all(exact.values()),
         "bitexact_layers": exact,
+        "output_sha256": digests,
         "layers": per_layer,
         "roofline": roofline,
         "cpu_baseline": cpu,
