@@ -119,7 +119,7 @@ def run_configs():
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     for cfg, name, M, N, K, std in CONFIGS:
-        x, w = synth.layer_inputs(M, N, K, seed=0, w_std=std, layer=hash(name) % 97)
+        x, w = synth.layer_inputs(M, N, K, seed=0, w_std=std, layer=_layer_id(name))
         xd = torch.from_numpy(x).to(dev)
         w0 = torch.from_numpy(w.view(np.int16)).to(dev)
         nrot = max(1, int(np.ceil(ROTATE_BYTES / (2.0 * N * K))))
@@ -201,7 +201,7 @@ def run_variant_configs():
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     for variant, name, M, N, K in VARIANT_CONFIGS:
-        layer = hash(name) % 97
+        layer = _layer_id(name)
         x = synth.normal_f32(M, K, 0, 1 + 16 * layer, 1.0)
         xd = torch.from_numpy(x).to(dev)
         if variant == "f32w":
@@ -642,6 +642,12 @@ def main():
         "baseline_scheme": scheme,
     }
     print(json.dumps(out), flush=True)
+
+
+def _layer_id(name):
+    """A stable per-layer stream id for the seeded inputs (str hash() is salted per process)."""
+    import zlib
+    return zlib.crc32(name.encode()) % 97
 
 
 def _kernel_hash():
