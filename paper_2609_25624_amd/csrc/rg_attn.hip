@@ -359,6 +359,145 @@ __global__ void __launch_bounds__(256) attn_partials_kernel(AttnArgs a) {
     }
 }
 
+// 3'. the same partials with one wave per work item (head dims 128 and 256).
+// Lane p owns the value columns 2p, 2p + 1 (and 2p + 128, 2p + 129 for D = 256)
+// for all G query heads of the group, so a value pair is read from LDS and
+// widened once and feeds 2G fmaf chains.  The item's positions are taken in
+// steps of RS = 32 (D = 128) or 16 (D = 256) rows (8 KB); the wave loads the
+// next step's value rows and scores into registers while it computes the
+// current step, and stages them in its own LDS region (waves never wait for
+// each other).  e for a step is computed into LDS as [position][head].  The
+// chains run over the valid positions only (the same values as chains over the
+// +0-padded segment).
+template <int G, int D>
+__global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
+    constexpr int RS = 4096 / D;                       // rows per step (8 KB of bf16)
+    constexpr int PPL = D / 128;                       // value pairs per lane
+    constexpr int GP = G <= 4 ? 4 : 8;                 // e row stride (floats)
+    constexpr int NVL = RS * D / 8 / 64;               // 16-byte vectors per lane per step (8)
+    constexpr int NTL = (RS * G + 63) / 64;            // scores per lane per step
+    __shared__ __attribute__((aligned(16))) uint16_t vs[4][RS * D];
+    __shared__ __attribute__((aligned(16))) float es[4][RS * GP];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int items = (int)(a.B * a.Hkv * a.J);
+    const int tw = (int)gridDim.x * 4;                 // waves in the grid
+    const int gw = (int)blockIdx.x * 4 + wave;
+    uint16_t* vw = vs[wave];
+    float* ew = es[wave];
+
+    // the wave's items gw, gw + tw, ... that hold positions
+    auto next = [&](int it) {
+        while (it < items && item_of(a, it).rows <= 0) it += tw;
+        return it;
+    };
+    uint4 vr[NVL];
+    float tr[NTL];
+    float mr[G];
+    auto fetch = [&](const Item& w, int s) {
+        const int r0 = s * RS;
+        const int nrow = min(RS, w.rows - r0);          // >= 1
+        const uint16_t* vb = a.v + (((int64_t)w.b * a.Hkv + w.g) * a.Lmax + w.l0 + r0) * D;
+#pragma unroll
+        for (int u = 0; u < NVL; ++u) {
+            const int i = lane + 64 * u;                // vector i: row i / (D / 8), column 8 (i % (D / 8))
+            const int row = i / (D / 8);
+            vr[u] = row < nrow ? *reinterpret_cast<const uint4*>(vb + (int64_t)row * D + 8 * (i % (D / 8)))
+                               : make_uint4(0u, 0u, 0u, 0u);
+        }
+        const int64_t tb = ((int64_t)w.b * a.H + (int64_t)w.g * G) * a.Lmax + w.l0 + r0;
+#pragma unroll
+        for (int u = 0; u < NTL; ++u) {
+            const int q = lane + 64 * u;                // (position q / G, head q % G)
+            const int l = q / G, h = q - l * G;
+            tr[u] = (q < RS * G && l < nrow) ? a.t[tb + (int64_t)h * a.Lmax + l] : 0.0f;
+        }
+        if (s == 0) {
+#pragma unroll
+            for (int h = 0; h < G; ++h) mr[h] = a.mmax[(int64_t)w.b * a.H + (int64_t)w.g * G + h];
+        }
+    };
+
+    int it = next(gw);
+    if (it >= items) return;
+    Item w = item_of(a, it);
+    int st = 0;
+    fetch(w, 0);
+    float n0[PPL][G], n1[PPL][G], ssum = 0.0f;
+    float mcur[G];
+    while (it < items) {
+        const Item cur = w;
+        const int ss = st;
+        const int nrow = min(RS, cur.rows - ss * RS);
+        // stage this step: value rows and e = EXP1(t - m) for the valid positions (+0 elsewhere)
+        if (ss == 0) {
+#pragma unroll
+            for (int h = 0; h < G; ++h) mcur[h] = mr[h];
+        }
+#pragma unroll
+        for (int u = 0; u < NVL; ++u) *reinterpret_cast<uint4*>(vw + 8 * (lane + 64 * u)) = vr[u];
+#pragma unroll
+        for (int u = 0; u < NTL; ++u) {
+            const int q = lane + 64 * u;
+            if (q < RS * G) {
+                const int l = q / G, h = q - l * G;
+                float mh = mcur[0];
+#pragma unroll
+                for (int i = 1; i < G; ++i) mh = (h == i) ? mcur[i] : mh;
+                ew[l * GP + h] = l < nrow ? exp1(tr[u] - mh) : 0.0f;
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        // next step (this item's, or the next item's first) in flight during the chains
+        if (st + 1 < (cur.rows + RS - 1) / RS) {
+            ++st;
+        } else {
+            st = 0;
+            it = next(it + tw);
+            if (it < items) w = item_of(a, it);
+        }
+        if (it < items) fetch(w, st);
+        if (ss == 0) {
+#pragma unroll
+            for (int k = 0; k < PPL; ++k)
+#pragma unroll
+                for (int h = 0; h < G; ++h) n0[k][h] = n1[k][h] = 0.0f;
+            ssum = 0.0f;
+        }
+        const float* es_own = ew + (lane < G ? lane : 0);
+#pragma unroll 4
+        for (int l = 0; l < nrow; ++l) {
+            float ev[G];
+#pragma unroll
+            for (int h = 0; h < G; ++h) ev[h] = ew[l * GP + h];
+#pragma unroll
+            for (int k = 0; k < PPL; ++k) {
+                const uint32_t v2 = *reinterpret_cast<const uint32_t*>(vw + l * D + 128 * k + 2 * lane);
+                const float vlo = __uint_as_float(v2 << 16), vhi = __uint_as_float(v2 & 0xffff0000u);
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    n0[k][h] = __builtin_fmaf(ev[h], vlo, n0[k][h]);
+                    n1[k][h] = __builtin_fmaf(ev[h], vhi, n1[k][h]);
+                }
+            }
+            ssum = ssum + es_own[l * GP];               // lanes < G: head `lane`'s segment sum
+        }
+        if (ss == (cur.rows + RS - 1) / RS - 1) {
+            const int64_t hb = (int64_t)cur.b * a.H + (int64_t)cur.g * G;
+#pragma unroll
+            for (int h = 0; h < G; ++h)
+#pragma unroll
+                for (int k = 0; k < PPL; ++k) {
+                    float* np = a.npart + ((hb + h) * a.J + cur.j) * D + 128 * k + 2 * lane;
+                    np[0] = n0[k][h];
+                    np[1] = n1[k][h];
+                }
+            if (lane < G) a.spart[(hb + lane) * a.J + cur.j] = ssum;
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
 // 4. out = N / S after the ascending folds of the segment partials.  Workgroup (b, h),
 // thread d.
 __global__ void __launch_bounds__(256) attn_fold_kernel(AttnArgs a) {
@@ -416,13 +555,32 @@ hipError_t launch_pair(K1 k1, int64_t lds1, K3 k3, int64_t lds3, const AttnArgs&
 
 // Fixed head dims (64, 128, 256): 64-column key steps and 16384 / D-row value steps
 // (32 KB tiles, four workgroups per CU).  Other D <= DM: one step of the whole segment.
+// D = 128 and 256 take the one-wave-per-item partials kernel (four 4-wave
+// workgroups per CU, each wave walking items gw, gw + waves, ...).
 template <int G, int D>
 hipError_t launch_fixed(const AttnArgs& a, int cus, hipStream_t stream) {
     constexpr int RS = 16384 / D;
     const int64_t lds1 = (int64_t)kAttnSeg * (64 + 8) * 2 + 16 * G;
-    const int64_t lds3 = (int64_t)G * kAttnSeg * 4 + (int64_t)RS * (D + 8) * 2;
-    return launch_pair(attn_scores_kernel<G, 64, D / 64, true>, lds1, attn_partials_kernel<G, D, RS, true>, lds3, a,
-                       cus, stream);
+    if constexpr (D == 128 || D == 256) {
+        const int64_t items = a.B * a.Hkv * a.J;
+        const int64_t g1 = items < (kLdsPerCU / lds1) * cus ? items : (kLdsPerCU / lds1) * cus;
+        const int64_t g3 = (items + 3) / 4 < 4 * (int64_t)cus ? (items + 3) / 4 : 4 * (int64_t)cus;
+        hipLaunchKernelGGL((attn_scores_kernel<G, 64, D / 64, true>), dim3((unsigned)g1), dim3(256), 0, stream, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(attn_max_kernel, dim3((unsigned)((a.B * a.H + 255) / 256)), dim3(256), 0, stream, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((attn_partials_wave_kernel<G, D>), dim3((unsigned)g3), dim3(256), 0, stream, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(attn_fold_kernel, dim3((unsigned)(a.B * a.H)), dim3(256), 0, stream, a);
+        return hipGetLastError();
+    } else {
+        const int64_t lds3 = (int64_t)G * kAttnSeg * 4 + (int64_t)RS * (D + 8) * 2;
+        return launch_pair(attn_scores_kernel<G, 64, D / 64, true>, lds1, attn_partials_kernel<G, D, RS, true>, lds3,
+                           a, cus, stream);
+    }
 }
 
 template <int G, int DM>
