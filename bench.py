@@ -19,6 +19,7 @@ import argparse
 import json
 import os
 import sys
+import re
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -361,7 +362,7 @@ def attn_trace_summary(path):
         blk = rows[c * per:(c + 1) * per][4 * 5:4 * (5 + 5 * 50)]       # the timed calls
         avg = {}
         for key in ("scores", "max", "partials", "fold"):
-            d = [dur(r) for r in blk if f"attn_{key}_" in r["Kernel_Name"]]
+            d = [dur(r) for r in blk if re.search(rf"attn_{key}\d?_", r["Kernel_Name"])]
             avg[key] = sum(d) / len(d)
         tot = sum(avg.values())
         kvb = 2 * B * Hkv * Lmax * D * 2

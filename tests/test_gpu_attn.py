@@ -62,6 +62,14 @@ def test_group_sizes(H, Hkv):
     _check(2, H, Hkv, 300, 64, [300, 41], seed=H * 10 + Hkv)
 
 
+@pytest.mark.parametrize("H,Hkv", [(1, 1), (3, 1), (8, 1), (16, 2), (7, 7)])
+@pytest.mark.parametrize("D", [128, 256])
+def test_group_sizes_at_the_wide_head_dims(H, Hkv, D):
+    """Group sizes at D = 128 and 256 (one wave per work item in the partials pass; the
+    two-positions-per-thread scores kernel for eight heads per kv head), ragged lengths."""
+    _check(3, H, Hkv, 600, D, [600, 257, 1], seed=H * 100 + Hkv + D)
+
+
 @pytest.mark.parametrize("D", [8, 16, 64, 96, 128, 136, 200, 256])
 def test_head_dims(D):
     _check(2, 4, 2, 520, D, [520, 257], seed=D, kstd=2.0)
