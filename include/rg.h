@@ -174,13 +174,16 @@ int rg_plan_f32w(int64_t M, int64_t N, int64_t K, rg_plan_t* out);
 /* Comparison point only (the scheme the paper improves on, Design, eq. 1):
  * w_f32[n][k] = up(W[n][k]) written to a caller-provided FP32 buffer of N*K
  * floats (the transient copy the fused kernel never makes).  Any FP32 GEMM
- * can then consume it.  Stream ordered, asynchronous. */
+ * can then consume it.  Stream ordered, asynchronous.  RG_ERR_INVAL for a
+ * null pointer or count < 1 (or count * 4 bytes overflowing), RG_ERR_ALIGN for
+ * a misaligned pointer, RG_ERR_ALIAS if the two buffers overlap. */
 int rg_cast_bf16_f32(const uint16_t* w_bf16, float* w_f32, int64_t count, void* stream);
 
 /* Greedy decision over logits (Evaluation, end-to-end determinism: argmax
  * returns the lower token id on a tie): out_idx[m] = the lowest n with
  * y[m][n] maximal, NaN never wins (all-NaN rows give -1).  y: device float32
- * [M][N]; out_idx: device int64 [M].  Deterministic; no atomics. */
+ * [M][N]; out_idx: device int64 [M], 8-byte aligned, must not overlap y
+ * (RG_ERR_ALIAS).  M <= 2^31 - 1.  Deterministic; no atomics. */
 int rg_argmax_rows(const float* y, int64_t* out_idx, int64_t M, int64_t N, void* stream);
 
 /* Test helpers: a stream restricted to the compute units set in `mask`

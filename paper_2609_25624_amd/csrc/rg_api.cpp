@@ -672,8 +672,9 @@ int rg_linear_bias(const float* x, const uint16_t* w, const float* bias, float* 
 }
 
 int rg_cast_bf16_f32(const uint16_t* w, float* o, int64_t count, void* stream) {
-    if (!w || !o || count < 1) return RG_ERR_INVAL;
+    if (!w || !o || count < 1 || !mul_ok(count, 1)) return RG_ERR_INVAL;
     if (((uintptr_t)w & 1) || ((uintptr_t)o & 3)) return RG_ERR_ALIGN;
+    if (overlaps(o, (size_t)count * 4, w, (size_t)count * 2)) return RG_ERR_ALIAS;
     const int dc = device_check(nullptr);
     if (dc != RG_OK) return dc;
     (void)hipGetLastError();
@@ -681,8 +682,9 @@ int rg_cast_bf16_f32(const uint16_t* w, float* o, int64_t count, void* stream) {
 }
 
 int rg_argmax_rows(const float* y, int64_t* out, int64_t M, int64_t N, void* stream) {
-    if (!y || !out || M < 1 || N < 1 || M > 2147483647) return RG_ERR_INVAL;
+    if (!y || !out || M < 1 || N < 1 || M > 2147483647 || !mul_ok(M, N)) return RG_ERR_INVAL;
     if (((uintptr_t)y & 3) || ((uintptr_t)out & 7)) return RG_ERR_ALIGN;
+    if (overlaps(out, (size_t)M * 8, y, (size_t)(M * N) * 4)) return RG_ERR_ALIAS;
     const int dc = device_check(nullptr);
     if (dc != RG_OK) return dc;
     (void)hipGetLastError();

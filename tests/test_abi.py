@@ -135,6 +135,12 @@ def test_other_entry_points_reject_bad_arguments():
     assert L.rg_cast_bf16_f32(0x1001, 0x1000, 10, None) == rg.RG_ERR_ALIGN
     assert L.rg_argmax_rows(0x1000, None, 1, 1, None) == rg.RG_ERR_INVAL
     assert L.rg_argmax_rows(0x1002, 0x2000, 1, 1, None) == rg.RG_ERR_ALIGN
+    # overflow of the sizes, and an output overlapping its input
+    assert L.rg_cast_bf16_f32(0x1000, 0x100000, 1 << 62, None) == rg.RG_ERR_INVAL
+    assert L.rg_cast_bf16_f32(0x1000, 0x1010, 16, None) == rg.RG_ERR_ALIAS
+    assert L.rg_argmax_rows(0x1000, 0x2000, 1 << 30, 1 << 40, None) == rg.RG_ERR_INVAL
+    assert L.rg_argmax_rows(0x1000, 0x1008, 2, 4, None) == rg.RG_ERR_ALIAS
+    assert L.rg_argmax_rows(0x1000, 0x1000 - 8, 2, 4, None) == rg.RG_ERR_ALIAS
     assert L.rg_stream_create_cu_mask(None, 1, None) == rg.RG_ERR_INVAL
     assert L.rg_stream_destroy(None) == rg.RG_ERR_INVAL
     assert L.rg_device_cu_count(None) == rg.RG_ERR_INVAL
