@@ -84,8 +84,8 @@ typedef enum {
  *   kernel        : -1/0 = planner's choice, else 1 + rg_kernel_id to force one
  *                   (a kernel that cannot handle the shape is not forced; the
  *                    call returns RG_ERR_RANGE)
- *   waves_per_wg  : 1..8  waves (64 threads each) per workgroup (gemv: 1..4, fewer
- *                   when x must fit in LDS beside the slots; ktile: 4, or 8 with tile_n 16)
+ *   waves_per_wg  : 1..8  waves (64 threads each) per workgroup (gemv: 1..4, and 1, 2
+ *                   or 4 when K > 4096; ktile: 4, or 8 with tile_n 16)
  *   grid_wgs      : 1..65536 workgroups (work is spread over them evenly)
  *   depth         : 2..3  decode pipeline depth in 128-byte-per-row slabs (unused by gemv);
  *                   tiled kernel with 128 x 128 tiles: the build for 2 or 3 waves per SIMD

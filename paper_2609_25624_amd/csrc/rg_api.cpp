@@ -134,43 +134,43 @@ bool decode_schedule(int64_t N, int64_t J, int mt, bool x_streamed, const rg_lau
 
 // Dense-stream M == 1 kernel: K a multiple of 256 with J >= 16 segments (64
 // lanes of a wave = 4 rows x 16 segments).  LDS per workgroup: a 32 KB slot
-// and 256 bytes of partials per wave, plus all of x (4K bytes).
-constexpr int64_t kLdsBytes = 160 * 1024 - 1024;
-constexpr int kGemvWaveLds = 32768 + 256;
-
-int gemv_max_waves(int64_t K) {
-    const int64_t nw = (kLdsBytes - 4 * K) / kGemvWaveLds;
-    return nw < 0 ? 0 : (nw > 4 ? 4 : (int)nw);
-}
+// and 256 bytes of partials per wave, plus a 16 KB x image (all of x for
+// K = 4096, else the current step's part), so four waves fit at any K.  With
+// J > 16 the waves of a workgroup share the x part and each DMAs the same
+// share of it: 1, 2 or 4 waves.
+constexpr int kGemvMaxWaves = 4;
 
 bool gemv_shape_ok(int64_t N, int64_t K) {
     return K % rg::kChunk == 0 && K / rg::kChunk >= 16 && K <= ((int64_t)1 << 26) &&
-           ceil_div(N, 4) < ((int64_t)1 << 31) && gemv_max_waves(K) >= 2;
+           ceil_div(N, 4) < ((int64_t)1 << 31);
 }
 
 // Waves and workgroups of the dense stream.  Default: the fewest rounds of
-// quads per wave that 256 workgroups of up to nwmax waves allow, then as few
-// waves as give that many rounds (every wave the same number of quads when
-// the shape allows), spread over as many workgroups as possible.
+// quads per wave that 256 workgroups of four waves allow, then as few waves
+// as give that many rounds (every wave the same number of quads when the
+// shape allows; 4 rather than 3 waves when J > 16), spread over as many
+// workgroups as possible.
 bool gemv_schedule(int64_t N, int64_t K, const rg_launch_t& o, Plan* p) {
-    const int nwmax = gemv_max_waves(K);
+    const bool xp = K / rg::kChunk != 16;
     const int64_t Q = ceil_div(N, 4);
     int nw = 0;
     int64_t G = 0;
     if (o.waves_per_wg > 0) {
-        if (o.waves_per_wg > nwmax) return false;
+        if (o.waves_per_wg > kGemvMaxWaves || (xp && o.waves_per_wg == 3)) return false;
         nw = o.waves_per_wg;
     }
     if (o.grid_wgs > 0) G = o.grid_wgs;
     if (nw == 0 && G == 0) {
-        const int64_t rounds = ceil_div(Q, (int64_t)kNominalCUs * nwmax);
+        const int64_t rounds = ceil_div(Q, (int64_t)kNominalCUs * kGemvMaxWaves);
         const int64_t vneed = ceil_div(Q, rounds);
         nw = (int)ceil_div(vneed, kNominalCUs);
+        if (xp && nw == 3) nw = 4;
         G = ceil_div(vneed, nw);
     } else if (nw == 0) {
         nw = (int)ceil_div(Q, G);
-        if (nw > nwmax) nw = nwmax;
+        if (nw > kGemvMaxWaves) nw = kGemvMaxWaves;
         if (nw < 1) nw = 1;
+        if (xp && nw == 3) nw = 4;
     } else if (G == 0) {
         G = ceil_div(Q, nw);
         if (G > kNominalCUs) G = kNominalCUs;

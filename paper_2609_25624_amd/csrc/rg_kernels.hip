@@ -1166,21 +1166,35 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
 // runs its whole 256-long fmaf chain from +0 inside the step.  The 4 lanes of
 // a DPP quad share a segment; lane r holds x for elements 64r .. 64r+63 of it
 // and the others read those through quad broadcasts fused into v_fmac_f32.
-// x stays in registers when one step covers K (K = 4096); otherwise the
-// workgroup keeps all of x in LDS and each lane reads its 64 values per step.
+// x stays in registers when one step covers K (K = 4096).  Otherwise (XP) the
+// workgroup stages x one step at a time: the 16 segments of step s (16 KB of
+// x) sit in a shared LDS image; at each step every wave reads its 64 values
+// into registers, the waves meet at a barrier, each wave DMAs its quarter
+// (NW = 4) of the next step's x into the image, and after its FMAs waits for
+// that DMA and meets the others at a second barrier.  All waves of a
+// workgroup therefore walk the same steps (a wave without a quad at some
+// round only moves x), and the 16 KB image leaves room for four 32 KB W
+// slots at any K.
 //
 // Order.  After a step the 16 segment partials of each row go to LDS and
 // lane r folds them into row r's running sum in ascending segment order
 // (the first partial starts the sum); after the quad's last step lane r
-// stores the row.
+// stores the row.  When one step covers K the partials of up to 8 quads are
+// kept and folded together, one row per lane, so the serial fold is paid
+// once per 8 quads instead of once per step.
 // ---------------------------------------------------------------------------
 constexpr int kGemvSlabBytes = 32768;   // 4 rows x 16 segments x 512 bytes of W
 
-template <int NW, bool XL>
+template <int NW, bool XP>
 __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
+    static_assert(!XP || 16 % NW == 0, "every wave issues the same number of x DMA instructions");
+    constexpr int XN = 16 / NW;   // XP: x DMA instructions per wave per step
     __shared__ __attribute__((aligned(16))) uint8_t wslot[NW][kGemvSlabBytes];
-    __shared__ __attribute__((aligned(16))) float fold[NW][64];   // [row r][segment j] of the step
-    extern __shared__ __attribute__((aligned(16))) uint8_t ximg[]; // x, K floats, swizzled
+    // partials [row r][segment j] of a step: of the last FB quads when one step covers K
+    // (folded FB quads at a time), else of the current step
+    constexpr int FB = XP ? 1 : 8;
+    __shared__ __attribute__((aligned(16))) float fold[NW][FB][64];
+    extern __shared__ __attribute__((aligned(16))) uint8_t ximg[]; // x (J == 16) or a step's part, 16 KB, swizzled
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -1231,31 +1245,48 @@ __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
         }
     };
 
-    // ---- x image, fetched by DMA ahead of the first W step and shared by the waves:
-    // 256-byte piece P = x[64P, 64P+64) at LDS 256P, its 16-byte slot i at slot i ^ (P & 15).
-    // Instruction b (1 KB) holds pieces 4b .. 4b+3; the waves take b = wave, wave + NW, ... ----
-    {
-        const uint32_t xbase = lds_addr(ximg);
+    // ---- x image, fetched by DMA and shared by the waves: 256-byte piece P = x[64P, 64P+64)
+    // (of all of x, or of the step's part) at LDS 256P, its 16-byte slot i at slot i ^ (P & 15).
+    // Instruction b (1 KB) holds pieces 4b .. 4b+3. ----
+    const uint32_t xbase = lds_addr(ximg);
+    // XP: part s = x[4096 s, 4096 s + 4096); wave w issues instructions w, w + NW, ... of its 16.
+    // Pieces past K (a short last part) copy the part's first piece and are never used.
+    auto issue_x = [&](int s) {
+        const int P0 = lane >> 4, sl = lane & 15;
+#pragma unroll
+        for (int i = 0; i < XN; ++i) {
+            const int bb = wave + NW * i;
+            const int P = 4 * bb + P0;
+            const int64_t e0 = 4096 * (int64_t)s + 64 * P;
+            const int64_t src = e0 < K ? e0 : 4096 * (int64_t)s;
+            dma16(a.x, (uint32_t)(4 * src + 16 * (sl ^ (P & 15))), xbase + 1024u * (uint32_t)bb);
+        }
+    };
+    // XP: every wave of the workgroup walks as many quads as its first wave owns (the most)
+    const int nq_wg = XP ? (int)a.qbase + ((int64_t)g * NW < a.qrem ? 1 : 0) : nq;
+    if constexpr (XP) {
+        if (nq_wg > 0) issue_x(0);
+        if (nq > 0) {
+            issue(0, 0);
+            vmcnt_wait<32>();     // this wave's part of x (issued first) has landed
+        } else {
+            vmcnt_wait<0>();
+        }
+    } else {
         const int nxi = (int)(K >> 8);
         const int P0 = lane >> 4, sl = lane & 15;
-        int pending = 0;
         for (int b = wave; b < nxi; b += NW) {
-            if (pending == 31) {      // keep this wave's outstanding operations (x + 32 W) within 63
-                vmcnt_wait<0>();
-                pending = 0;
-            }
             const int P = 4 * b + P0;
             dma16(a.x, (uint32_t)(256 * P + 16 * (sl ^ (P & 15))), xbase + 1024u * (uint32_t)b);
-            ++pending;
+        }
+        if (nq > 0) {
+            issue(0, 0);
+            vmcnt_wait<32>();     // this wave's x instructions (issued first) have landed
+        } else {
+            vmcnt_wait<0>();
         }
     }
-    if (nq > 0) {
-        issue(0, 0);
-        vmcnt_wait<32>();     // this wave's x instructions (issued first) have landed
-    } else {
-        vmcnt_wait<0>();
-    }
-    __syncthreads();          // the whole x image is in LDS
+    __syncthreads();          // the x image is in LDS
 
     // lane c reads x piece P (segment P / 4, part P % 4) into X[0..63]
     float X[64];
@@ -1270,88 +1301,141 @@ __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
             X[4 * i + 3] = t4.w;
         }
     };
-    if constexpr (!XL) load_x(lane);   // one step covers K: the same x every step
+    if constexpr (!XP) load_x(lane);   // one step covers K: the same x every step
 
     const int sw = (lane >> 1) & 7;
     const uint8_t* rd = &wslot[wave][128 * lane];
     float yrun = 0.0f;   // lanes 0..3: running fold of row `lane` of the current quad
 
-    for (int t = 0; t < nq; ++t) {
+    for (int t = 0; t < nq_wg; ++t) {
         for (int s = 0; s < S; ++s) {
-            const bool more = (s + 1 < S) || (t + 1 < nq);
-            // x for segment 16s + j, part r: piece P = 64s + lane (present segments only)
-            if constexpr (XL) load_x((16 * s + (lane >> 2) < J) ? 64 * s + lane : lane);
-            float acc = 0.0f;
-            auto chain8 = [&](auto qc, const uint4& p, int u) {
-                constexpr int q = decltype(qc)::value;
-                const uint32_t d[4] = {p.x, p.y, p.z, p.w};
-                float wv[8];
-#pragma unroll
-                for (int h = 0; h < 8; ++h) wv[h] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
-                fmac8_bcast<q>(acc, &X[8 * u], wv);
-            };
-            if (more) {
-                // whole step to registers, request the next one into the freed slot, then the chains
-                vmcnt_wait<0>();
-                uint4 wp[32];
-#pragma unroll
-                for (int i = 0; i < 32; ++i)
-                    wp[i] = *reinterpret_cast<const uint4*>(rd + 8192 * (i >> 3) + 16 * ((i & 7) ^ sw));
-                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-                issue(s + 1 < S ? t : t + 1, s + 1 < S ? s + 1 : 0);
-#pragma unroll
-                for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 0>{}, wp[u], u);
-#pragma unroll
-                for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 1>{}, wp[8 + u], u);
-#pragma unroll
-                for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 2>{}, wp[16 + u], u);
-#pragma unroll
-                for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 3>{}, wp[24 + u], u);
-            } else {
-                // this wave's last step: consume each quarter as its 8 DMA instructions land
-                // (at most 8 * (3 - q) of the step's instructions outstanding; later
-                // operations only add slack)
-                auto quarter = [&](auto qc) {
+            const bool act = t < nq;                              // this wave has a quad at round t
+            const bool more = act && ((s + 1 < S) || (t + 1 < nq));
+            bool xn = false;                                      // XP: the next step's x was requested
+            if constexpr (XP) {
+                load_x(lane);                                     // piece `lane` of the step's part
+                __syncthreads();                                  // every wave has read the image
+                xn = (s + 1 < S) || (t + 1 < nq_wg);
+                if (xn) issue_x(s + 1 < S ? s + 1 : 0);
+            }
+            if (act) {
+                float acc = 0.0f;
+                auto chain8 = [&](auto qc, const uint4& p, int u) {
                     constexpr int q = decltype(qc)::value;
-                    vmcnt_wait<8 * (3 - q)>();
-                    uint4 wp[8];
+                    const uint32_t d[4] = {p.x, p.y, p.z, p.w};
+                    float wv[8];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u)
-                        wp[u] = *reinterpret_cast<const uint4*>(rd + 8192 * q + 16 * (u ^ sw));
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) chain8(qc, wp[u], u);
+                    for (int h = 0; h < 8; ++h) wv[h] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+                    fmac8_bcast<q>(acc, &X[8 * u], wv);
                 };
-                quarter(std::integral_constant<int, 0>{});
-                quarter(std::integral_constant<int, 1>{});
-                quarter(std::integral_constant<int, 2>{});
-                quarter(std::integral_constant<int, 3>{});
-            }
+                if (more) {
+                    // whole step to registers, request the next one into the freed slot, then the
+                    // chains (the step's DMA is everything but the x part issued after it)
+                    if (xn) vmcnt_wait<XN>();
+                    else vmcnt_wait<0>();
+                    uint4 wp[32];
+#pragma unroll
+                    for (int i = 0; i < 32; ++i)
+                        wp[i] = *reinterpret_cast<const uint4*>(rd + 8192 * (i >> 3) + 16 * ((i & 7) ^ sw));
+                    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                    issue(s + 1 < S ? t : t + 1, s + 1 < S ? s + 1 : 0);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 0>{}, wp[u], u);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 1>{}, wp[8 + u], u);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 2>{}, wp[16 + u], u);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) chain8(std::integral_constant<int, 3>{}, wp[24 + u], u);
+                } else {
+                    // this wave's last step: consume each quarter as its 8 DMA instructions land
+                    // (at most 8 * (3 - q) of the step's instructions outstanding, plus an x part
+                    // issued after them; later operations only add slack)
+                    auto quarter = [&](auto qc) {
+                        constexpr int q = decltype(qc)::value;
+                        if (xn) vmcnt_wait<8 * (3 - q) + (XP ? XN : 0)>();
+                        else vmcnt_wait<8 * (3 - q)>();
+                        uint4 wp[8];
+#pragma unroll
+                        for (int u = 0; u < 8; ++u)
+                            wp[u] = *reinterpret_cast<const uint4*>(rd + 8192 * q + 16 * (u ^ sw));
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) chain8(qc, wp[u], u);
+                    };
+                    quarter(std::integral_constant<int, 0>{});
+                    quarter(std::integral_constant<int, 1>{});
+                    quarter(std::integral_constant<int, 2>{});
+                    quarter(std::integral_constant<int, 3>{});
+                }
 
-            // ascending fold of the step's segment partials into each row's sum
-            fold[wave][16 * (lane & 3) + (lane >> 2)] = acc;
-            __builtin_amdgcn_wave_barrier();
-            if (lane < 4) {
-                float p[16];
+                if constexpr (!XP) {
+                    // one step per quad: keep the quad's 64 partials and fold FB quads at once,
+                    // lane 4 qq + r taking row r of the batch's quad qq (16 partials, ascending)
+                    const int fq = t % FB;
+                    fold[wave][fq][16 * (lane & 3) + (lane >> 2)] = acc;
+                    if (fq == FB - 1 || t == nq - 1) {
+                        __builtin_amdgcn_wave_barrier();
+                        if (lane < 4 * (fq + 1)) {
+                            const int qq = lane >> 2, r = lane & 3;
+                            float p[16];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float4 t4 = *reinterpret_cast<const float4*>(&fold[wave][16 * lane + 4 * i]);
-                    p[4 * i + 0] = t4.x;
-                    p[4 * i + 1] = t4.y;
-                    p[4 * i + 2] = t4.z;
-                    p[4 * i + 3] = t4.w;
-                }
-                const int jn = min(16, J - 16 * s);
-                float y = (s == 0) ? p[0] : yrun + p[0];
+                            for (int i = 0; i < 4; ++i) {
+                                const float4 t4 = *reinterpret_cast<const float4*>(&fold[wave][qq][16 * r + 4 * i]);
+                                p[4 * i + 0] = t4.x;
+                                p[4 * i + 1] = t4.y;
+                                p[4 * i + 2] = t4.z;
+                                p[4 * i + 3] = t4.w;
+                            }
+                            float y = p[0];
 #pragma unroll
-                for (int i = 1; i < 16; ++i)
-                    if (i < jn) y = y + p[i];
-                yrun = y;
-                if (s == S - 1) {
-                    const int64_t n = 4 * (v + (int64_t)t * V) + lane;
-                    if (n < N) a.y[n] = a.bias ? y + a.bias[n] : y;
+                            for (int i = 1; i < 16; ++i) y = y + p[i];
+                            const int64_t n = 4 * (v + (int64_t)(t - fq + qq) * V) + r;
+                            if (n < N) a.y[n] = a.bias ? y + a.bias[n] : y;
+                        }
+                        __builtin_amdgcn_wave_barrier();
+                    }
+                } else {
+                    // ascending fold of the step's segment partials into each row's running sum
+                    fold[wave][0][16 * (lane & 3) + (lane >> 2)] = acc;
+                    __builtin_amdgcn_wave_barrier();
+                    if (lane < 4) {
+                        float p[16];
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float4 t4 = *reinterpret_cast<const float4*>(&fold[wave][0][16 * lane + 4 * i]);
+                            p[4 * i + 0] = t4.x;
+                            p[4 * i + 1] = t4.y;
+                            p[4 * i + 2] = t4.z;
+                            p[4 * i + 3] = t4.w;
+                        }
+                        const int jn = min(16, J - 16 * s);
+                        float y = (s == 0) ? p[0] : yrun + p[0];
+                        if (jn == 16) {
+#pragma unroll
+                            for (int i = 1; i < 16; ++i) y = y + p[i];
+                        } else {
+#pragma unroll
+                            for (int i = 1; i < 16; ++i)
+                                if (i < jn) y = y + p[i];
+                        }
+                        yrun = y;
+                        if (s == S - 1) {
+                            const int64_t n = 4 * (v + (int64_t)t * V) + lane;
+                            if (n < N) a.y[n] = a.bias ? y + a.bias[n] : y;
+                        }
+                    }
+                    __builtin_amdgcn_wave_barrier();
                 }
             }
-            __builtin_amdgcn_wave_barrier();
+            if constexpr (XP) {
+                // this wave's part of the next x has landed (only the next W step, requested
+                // after it, may be outstanding), then every wave's has
+                if (xn) {
+                    if (more) vmcnt_wait<32>();
+                    else vmcnt_wait<0>();
+                }
+                __syncthreads();
+            }
         }
     }
 }
@@ -1630,26 +1714,30 @@ hipError_t launch_decode1(const DecodeArgs& a, int grid, int nw, int depth, hipS
     }
 }
 
-template <int NW, bool XL>
+template <int NW, bool XP>
 static hipError_t launch_gemv_t(const GemvArgs& a, int grid, hipStream_t stream) {
-    const size_t dyn = (size_t)a.K * sizeof(float);   // the x image
-    hipLaunchKernelGGL((gemv_kernel<NW, XL>), dim3(grid), dim3(NW * 64), dyn, stream, a);
+    const size_t dyn = 4096 * sizeof(float);   // the x image: all of x (K = 4096) or a step's part
+    hipLaunchKernelGGL((gemv_kernel<NW, XP>), dim3(grid), dim3(NW * 64), dyn, stream, a);
     return hipGetLastError();
 }
 
-// M == 1 dense stream: 1..4 waves of 32 KB slots beside the x image; x pieces
-// held in registers for the whole kernel when J == 16, else re-read every step.
+// M == 1 dense stream: 1..4 waves of 32 KB slots beside a 16 KB x image; x
+// pieces held in registers for the whole kernel when J == 16, else staged a
+// step at a time (1, 2 or 4 waves).
 hipError_t launch_gemv(const GemvArgs& a, int grid, int nw, hipStream_t stream) {
-    const bool xl = a.J != 16;
-    switch (nw * 2 + (xl ? 1 : 0)) {
-        case 2: return launch_gemv_t<1, false>(a, grid, stream);
-        case 3: return launch_gemv_t<1, true>(a, grid, stream);
-        case 4: return launch_gemv_t<2, false>(a, grid, stream);
-        case 5: return launch_gemv_t<2, true>(a, grid, stream);
-        case 6: return launch_gemv_t<3, false>(a, grid, stream);
-        case 7: return launch_gemv_t<3, true>(a, grid, stream);
-        case 8: return launch_gemv_t<4, false>(a, grid, stream);
-        case 9: return launch_gemv_t<4, true>(a, grid, stream);
+    if (a.J == 16) {
+        switch (nw) {
+            case 1: return launch_gemv_t<1, false>(a, grid, stream);
+            case 2: return launch_gemv_t<2, false>(a, grid, stream);
+            case 3: return launch_gemv_t<3, false>(a, grid, stream);
+            case 4: return launch_gemv_t<4, false>(a, grid, stream);
+            default: return hipErrorInvalidValue;
+        }
+    }
+    switch (nw) {
+        case 1: return launch_gemv_t<1, true>(a, grid, stream);
+        case 2: return launch_gemv_t<2, true>(a, grid, stream);
+        case 4: return launch_gemv_t<4, true>(a, grid, stream);
         default: return hipErrorInvalidValue;
     }
 }

@@ -68,15 +68,17 @@ def test_gemv_schedule_defaults():
         assert (p["grid_wgs"], p["waves_per_wg"]) == (256, 3)
         p = rg.rg_plan(1, 28672, 4096)           # 7168 quads: seven rounds of 1024 waves
         assert (p["grid_wgs"], p["waves_per_wg"]) == (256, 4)
-        p = rg.rg_plan(1, 4096, 14336)           # x (56 KB) in LDS leaves room for 3 slots
-        assert p["waves_per_wg"] <= 3
+        p = rg.rg_plan(1, 4096, 14336)           # x staged a step at a time: four slots fit at any K
+        assert (p["grid_wgs"], p["waves_per_wg"]) == (256, 4)
+        p = rg.rg_plan(1, 3072, 8192)            # 768 quads: 3 waves would do, K > 4096 takes 4
+        assert (p["grid_wgs"], p["waves_per_wg"]) == (192, 4)
     finally:
         rg.rg_linear_set_launch(None)
-    rg.rg_linear_set_launch(kernel="gemv", waves_per_wg=4)
+    rg.rg_linear_set_launch(kernel="gemv", waves_per_wg=3)
     try:
         with pytest.raises(rg.RgError):
-            rg.rg_plan(1, 4096, 14336)           # 4 slots + x do not fit
-        assert rg.rg_plan(1, 4096, 4096)["waves_per_wg"] == 4
+            rg.rg_plan(1, 4096, 14336)           # K > 4096: the waves share the x part in 1, 2 or 4 shares
+        assert rg.rg_plan(1, 4096, 4096)["waves_per_wg"] == 3
     finally:
         rg.rg_linear_set_launch(None)
     rg.rg_linear_set_launch(waves_per_wg=4)     # not forced: another kernel takes the shape

@@ -212,6 +212,26 @@ def test_gemv_shapes(N, K):
         rg.rg_linear_set_launch(None)
 
 
+@pytest.mark.parametrize("N,K,cfg", [
+    (4120, 8192, dict()),                                   # 1030 quads on 129 x 4 waves: 2 or 1 each
+    (4120, 12544, dict(waves_per_wg=4, grid_wgs=7)),        # 36-37 quads per wave, last step 1 segment
+    (4096, 14336, dict()),                                  # one quad per wave, 3.5 steps
+    (2049, 5120, dict(waves_per_wg=2, grid_wgs=300, grid_order=1)),   # empty workgroups
+    (13, 8448, dict(waves_per_wg=1)),
+])
+def test_gemv_staged_x(N, K, cfg):
+    """M = 1 dense stream with K > 4096: the workgroup's waves share each step's x part through
+    LDS and walk the same steps; waves with fewer quads only move x in the rounds they sit out."""
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(kernel="gemv", **cfg)
+    try:
+        p = rg.rg_plan(1, N, K)
+        gu.log(f"gemv staged x N={N} K={K} {cfg} -> waves {p['waves_per_wg']} grid {p['grid_wgs']}")
+        _check_layer(1, N, K, seed=N ^ K)
+    finally:
+        rg.rg_linear_set_launch(None)
+
+
 @pytest.mark.parametrize("M,kernel", [(1, "decode_xs"), (1, "decode"), (2, "decode")])
 @pytest.mark.parametrize("N,K", [(1030, 4096), (4097, 1000), (515, 14336), (6141, 4352)])
 @pytest.mark.parametrize("grid,order", [(3, 0), (7, 1), (13, 0)])
