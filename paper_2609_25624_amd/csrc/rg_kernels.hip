@@ -544,7 +544,8 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
 // 16e+16) of the slab; the others reach it through DPP quad broadcasts.  The
 // 256-byte x image of a quad is stored with its 16-byte pieces permuted
 // (piece c of lane e at slot 4e + (c ^ (quad & 3))) so that the 16 lanes of
-// an LDS phase read 16 distinct bank groups.
+// an LDS phase read 16 distinct bank groups.  The segment partials of up to
+// 4 rounds are kept in LDS and folded together, one row per thread.
 // ---------------------------------------------------------------------------
 constexpr int kXSlabBytesPerWave = 16 * 256;  // 4 KB: 16 quads x 64 floats
 
@@ -597,7 +598,8 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
 
     __shared__ __attribute__((aligned(16))) uint8_t wring[NW][DEPTH][kSlabBytesPerWave];
     __shared__ __attribute__((aligned(16))) uint8_t xring[NW][DEPTH][kXSlabBytesPerWave];
-    __shared__ float part[2][kThreads];               // [parity][row_local * J + j]
+    constexpr int FR = 4;                             // rounds whose partials are folded together
+    __shared__ float part[FR][kThreads];              // [round % FR][row_local * J + j]
     extern __shared__ float yres[];                   // [row_in_wg], dynamic
 
     const int tid = threadIdx.x;
@@ -744,12 +746,20 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
             else fma_slab1<false>(wp, Xs, acc, npieces);
         }
         if (s == 3) {
-            const int par = r & 1;
-            if (active) part[par][(4 * lq + e) * J + jj] = acc;
-            __syncthreads();
-            const int rows_round = 4 * min(RQ, nq - r * RQ);
-            for (int o = tid; o < rows_round; o += kThreads)
-                yres[r * RQ * 4 + o] = fold_partials(&part[par][o * J], J);
+            // keep the round's partials; every FR rounds (and after the last) fold them all,
+            // one row per thread, so the serial fold is waited for once per FR rounds
+            const int slot = r % FR;
+            if (active) part[slot][(4 * lq + e) * J + jj] = acc;
+            if (slot == FR - 1 || r == rounds - 1) {
+                __syncthreads();
+                const int r0 = r - slot;
+                const int rows = 4 * min((slot + 1) * RQ, nq - r0 * RQ);
+                for (int o = tid; o < rows; o += kThreads) {
+                    const int rr = o / (4 * RQ), ro = o - rr * 4 * RQ;
+                    yres[r0 * RQ * 4 + o] = fold_partials(&part[rr][ro * J], J);
+                }
+                __syncthreads();                      // the next round writes the ring again
+            }
         }
     }
     vmcnt_wait<0>();
