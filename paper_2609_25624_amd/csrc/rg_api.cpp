@@ -134,8 +134,9 @@ bool decode_schedule(int64_t N, int64_t J, int mt, bool x_streamed, const rg_lau
 
 // Dense-stream M == 1 kernel: K a multiple of 256 with J >= 16 segments (64
 // lanes of a wave = 4 rows x 16 segments).  LDS per workgroup: a 32 KB slot
-// and 256 bytes of partials per wave, plus a 16 KB x image (all of x for
-// K = 4096, else the current step's part), so four waves fit at any K.  With
+// and 2 KB of partials per wave (256 bytes when K > 4096), plus a 16 KB x
+// image (all of x for K = 4096, else the current step's part), so four waves
+// fit at any K.  With
 // J > 16 the waves of a workgroup share the x part and each DMAs the same
 // share of it: 1, 2 or 4 waves.
 constexpr int kGemvMaxWaves = 4;
