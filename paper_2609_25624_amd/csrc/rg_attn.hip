@@ -16,9 +16,11 @@
 //                ascending order; values and e staged in LDS).
 //   4. fold:     workgroup (b, h) folds the S_j and n_j[d] in ascending j and
 //                divides.
-// Kernels 1 and 3 are persistent: a workgroup walks work items it, it + grid,
-// ... in steps of one 32 KB tile (for the usual head dims), and fetches the next
-// step's tile into registers while it computes the current one from LDS.
+// Kernels 1 and 3 are persistent: a workgroup (kernel 1; kernel 3 for head dims
+// other than 128 and 256) walks work items it, it + grid, ... in steps of one
+// 32 KB tile (for the usual head dims), or for kernel 3 with head dims 128 and
+// 256 a single wave walks them in 8 KB steps; either fetches the next step into
+// registers while it computes the current one from LDS.
 // Arithmetic: binary32 fmaf / add / multiply / correctly rounded divide,
 // denormals kept, no contraction (the build uses -ffp-contract=off).
 
@@ -31,8 +33,6 @@ namespace rg {
 namespace {
 
 constexpr int kAttnSeg = 256;                 // positions per segment
-
-__device__ __forceinline__ float up_bf16(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 // EXP1 of include/rg_attn.h.
 __device__ __forceinline__ float exp1(float u) {
@@ -667,8 +667,9 @@ hipError_t launch_pair(K1 k1, int64_t lds1, K3 k3, int64_t lds3, const AttnArgs&
 
 // Fixed head dims (64, 128, 256).  Scores: 64-column key steps (32 KB tiles, four
 // workgroups per CU); with eight query heads per kv head the two-positions-per-
-// thread kernel (32-column steps, 128 threads, about 20 KB of LDS; measured 7 %
-// faster there, 0-22 % slower with six or fewer heads).  Partials: one wave per
+// thread kernel (32-column steps, 128 threads, about 20 KB of LDS; measured
+// 111 -> 90 us for the scores of a 32 x 64-head, 4096-position batch, and 0-22 %
+// slower than the 64-column kernel with six or fewer heads).  Partials: one wave per
 // work item for D = 128 and 256 (four 4-wave workgroups per CU, each wave walking
 // items gw, gw + waves, ...); for D = 64 the workgroup-per-item kernel with
 // 16384 / D-row value steps (32 KB tiles, four workgroups per CU).  Other D <= DM:
