@@ -37,8 +37,12 @@
  * Threading and streams.  Calls are asynchronous and stream ordered on the
  * given stream (a hipStream_t passed as void*; NULL = the null stream).  The
  * library never synchronizes and allocates no device memory in rg_linear.
- * Concurrent calls on different streams are safe.  rg_linear_set_launch is
- * process global and not thread safe (a test knob).
+ * Concurrent calls from several threads, on the same or different streams,
+ * are safe.  rg_linear_set_launch changes one process-wide setting (a test
+ * knob, updated under a lock) that every later call of every thread uses;
+ * since launch settings never change the arithmetic, a call racing with it
+ * still returns the same bits, or RG_ERR_RANGE if the setting it read does
+ * not fit its shape.
  *
  * Errors.  Every entry point returns an rg_status code; none aborts or prints.
  */
