@@ -112,6 +112,10 @@ def _tensor_ptr(t, dtypes, name):
         raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous (row-major)")
+    cur = torch.cuda.current_device()
+    if t.device.index != cur:
+        # the library launches on the current device; memory of another device is not passed on
+        raise ValueError(f"{name} is on {t.device} but the current device is cuda:{cur}")
     return t.data_ptr()
 
 
