@@ -262,6 +262,8 @@ ATTN_CONFIGS = [  # (name, B, H, Hkv, Lmax, D)
 
 
 def run_attention_configs():
+    import hashlib
+
     import numpy as np
     import torch
 
@@ -308,7 +310,8 @@ def run_attention_configs():
             "variant": "attention", "config": name, "B": B, "H": H, "Hkv": Hkv, "L": Lmax, "D": D,
             "us_per_call": round(us, 3), "kv_bytes": int(kvb), "kv_TBs": round(kvb / (us * 1e-6) / 1e12, 4),
             "frac_of_8TBs": round(kvb / (us * 1e-6) / (HBM_PEAK_GBS * 1e9), 4), "bitexact": exact,
-            "checked": "all", "rotated_copies": nrot}), flush=True)
+            "checked": "all", "rotated_copies": nrot,
+            "output_sha256": hashlib.sha256(np.ascontiguousarray(got).tobytes()).hexdigest()[:16]}), flush=True)
         del kds, vds, ws, qd
         torch.cuda.empty_cache()
 
