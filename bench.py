@@ -354,18 +354,25 @@ def trace_summary(path, args):
 
 def attn_trace_summary(path):
     """Per-configuration kernel durations from a rocprofv3 kernel trace of 'bench.py --attention'.
-    Each configuration makes 5 + 5 * 50 + 1 calls of four kernels, in ATTN_CONFIGS order."""
+    Each configuration makes 5 + 5 * 50 + 1 calls, in ATTN_CONFIGS order; a call is three or four
+    kernels (the per-row maximum is its own kernel only for some shapes) and starts with the
+    scores kernel."""
     rows = [r for r in _csv_rows(path) if "attn_" in r["Kernel_Name"]]
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
     dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-    per = 4 * (5 + 5 * 50 + 1)
-    print(f"dispatches of the attention kernels: {len(rows)}")
+    calls = []
+    for r in rows:
+        if re.search(r"attn_scores\d?_", r["Kernel_Name"]) or not calls:
+            calls.append([])
+        calls[-1].append(r)
+    per = 5 + 5 * 50 + 1
+    print(f"dispatches of the attention kernels: {len(rows)} in {len(calls)} calls")
     print(f"{'config':22s} {'scores_us':>10s} {'max_us':>8s} {'partials_us':>12s} {'fold_us':>8s} {'sum_us':>8s} {'KV TB/s':>8s}")
     for c, (name, B, H, Hkv, Lmax, D) in enumerate(ATTN_CONFIGS):
-        blk = rows[c * per:(c + 1) * per][4 * 5:4 * (5 + 5 * 50)]       # the timed calls
+        timed = calls[c * per:(c + 1) * per][5:5 + 5 * 50]
         avg = {}
         for key in ("scores", "max", "partials", "fold"):
-            d = [dur(r) for r in blk if re.search(rf"attn_{key}\d?_", r["Kernel_Name"])]
+            d = [sum(dur(r) for r in call if re.search(rf"attn_{key}\d?_", r["Kernel_Name"])) for call in timed]
             avg[key] = sum(d) / len(d)
         tot = sum(avg.values())
         kvb = 2 * B * Hkv * Lmax * D * 2

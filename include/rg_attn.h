@@ -75,9 +75,10 @@ int64_t rg_attn_workspace_size(int64_t B, int64_t H, int64_t Lmax, int64_t D);
  *   scale: multiplies each score after the dot product (e.g. 1/sqrt(D) as a float)
  *   workspace_bytes >= rg_attn_workspace_size(B, H, Lmax, D); its contents on
  *     entry do not matter and are overwritten
- * out must not overlap q, kc, vc, lens or the workspace.  Four kernels are
- * enqueued on `stream` (scores and segment maxima; the maximum per row;
- * exponentials and segment partials; the ascending folds and the division).  Returns RG_OK, or
+ * out must not overlap q, kc, vc, lens or the workspace.  Three or four kernels
+ * are enqueued on `stream` (scores and segment maxima; the maximum per row,
+ * which for some shapes the next kernel takes itself; exponentials and segment
+ * partials; the ascending folds and the division).  Returns RG_OK, or
  * RG_ERR_INVAL / RG_ERR_ALIGN / RG_ERR_ALIAS / RG_ERR_ARCH / RG_ERR_HIP as rg.h.
  */
 int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const int32_t* lens, float* out,

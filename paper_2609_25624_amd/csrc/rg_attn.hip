@@ -1,15 +1,17 @@
 // Fixed-order decode attention kernels for gfx950 (MI355X): the order
 // RG-ATTN-1 and its exponential EXP1, both defined in include/rg_attn.h.
 //
-// Four launches, each deterministic by construction (no atomics, no order
-// that depends on the grid):
+// Four launches (three when the partials kernel takes the row maxima itself),
+// each deterministic by construction (no atomics, no order that depends on the
+// grid):
 //   1. scores:   work item (b, g, j) = segment j (positions [256j, 256j + 256))
 //                of kv head g of sequence b; its keys are staged in LDS and
 //                thread l runs the dot product chain of position l for every
 //                query head of the group, scales it, writes t, and the
 //                workgroup writes the segment's maximum per head (max is
 //                exact, so its tree shape does not matter).
-//   2. max:      m[b][h] = the largest segment maximum.
+//   2. max:      m[b][h] = the largest segment maximum (exact, so it is the same
+//                value when the partials kernel reduces it per item instead).
 //   3. partials: per work item, e_l = EXP1(t_l - m), the segment sum S_j (one
 //                addition chain per head) and the segment numerators n_j[d]
 //                (one fmaf chain per head and d over the positions in
@@ -480,8 +482,10 @@ __global__ void __launch_bounds__(256) attn_partials_kernel(AttnArgs a) {
 // current step, and stages them in its own LDS region (waves never wait for
 // each other).  e for a step is computed into LDS as [position][head].  The
 // chains run over the valid positions only (the same values as chains over the
-// +0-padded segment).
-template <int G, int D>
+// +0-padded segment).  INMAX: the wave takes its item's row maxima from the
+// segment maxima itself (the largest one per head, exact), so the maximum kernel
+// is not launched; used when no wave has more than one item.
+template <int G, int D, bool INMAX>
 __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
     constexpr int RS = 4096 / D;                       // rows per step (8 KB of bf16)
     constexpr int PPL = D / 128;                       // value pairs per lane
@@ -505,6 +509,11 @@ __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
     };
     uint4 vr[NVL];
     float tr[NTL];
+    // INMAX: the first 512 of the item's G * Jb segment maxima are loaded with its first
+    // step into smv and reduced before its exponentials; lane-local maxima of any further
+    // values (sequences longer than 512 / G segments) are taken at once into mr.  When G
+    // divides 64, lane l only ever holds values of head l % G, kept in mr[0].
+    float smv[INMAX ? 8 : 1];
     float mr[G];
     auto fetch = [&](const Item& w, int s) {
         const int r0 = s * RS;
@@ -525,8 +534,34 @@ __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
             tr[u] = (q < RS * G && l < nrow) ? a.t[tb + (int64_t)h * a.Lmax + l] : 0.0f;
         }
         if (s == 0) {
+            if constexpr (INMAX) {
+                const int jb = (w.L + kAttnSeg - 1) / kAttnSeg;
+                const float* smb = a.segmax + ((int64_t)w.b * a.H + (int64_t)w.g * G) * a.J;   // head h at h * J
+                const int snv = G * jb;
 #pragma unroll
-            for (int h = 0; h < G; ++h) mr[h] = a.mmax[(int64_t)w.b * a.H + (int64_t)w.g * G + h];
+                for (int u = 0; u < 8; ++u) {
+                    const int idx = lane + 64 * u;
+                    smv[u] = idx < snv ? smb[(int64_t)(idx % G) * a.J + idx / G] : -__builtin_inff();
+                }
+#pragma unroll
+                for (int h = 0; h < G; ++h) mr[h] = -__builtin_inff();
+                for (int base = 512; base < snv; base += 64) {
+                    const int idx = base + lane;
+                    if (idx < snv) {
+                        const float v = smb[(int64_t)(idx % G) * a.J + idx / G];
+                        if constexpr (64 % G == 0) {
+                            mr[0] = __builtin_fmaxf(mr[0], v);
+                        } else {
+                            const int h = idx % G;
+#pragma unroll
+                            for (int i = 0; i < G; ++i) mr[i] = (h == i) ? __builtin_fmaxf(mr[i], v) : mr[i];
+                        }
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int h = 0; h < G; ++h) mr[h] = a.mmax[(int64_t)w.b * a.H + (int64_t)w.g * G + h];
+            }
         }
     };
 
@@ -543,8 +578,36 @@ __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
         const int nrow = min(RS, cur.rows - ss * RS);
         // stage this step: value rows and e = EXP1(t - m) for the valid positions (+0 elsewhere)
         if (ss == 0) {
+            if constexpr (!INMAX) {
 #pragma unroll
-            for (int h = 0; h < G; ++h) mcur[h] = mr[h];
+                for (int h = 0; h < G; ++h) mcur[h] = mr[h];
+            } else if constexpr (64 % G == 0) {
+                // reduce over the lanes of each head, then take head h's maximum from lane h
+                float ml = mr[0];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) ml = __builtin_fmaxf(ml, smv[u]);
+#pragma unroll
+                for (int sh = 32; sh >= G; sh >>= 1) ml = __builtin_fmaxf(ml, __shfl_xor(ml, sh, 64));
+#pragma unroll
+                for (int h = 0; h < G; ++h)
+                    mcur[h] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ml), h));
+            } else {
+                float ml[G];
+#pragma unroll
+                for (int h = 0; h < G; ++h) ml[h] = mr[h];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int h = (lane + 64 * u) % G;
+#pragma unroll
+                    for (int i = 0; i < G; ++i) ml[i] = (h == i) ? __builtin_fmaxf(ml[i], smv[u]) : ml[i];
+                }
+#pragma unroll
+                for (int sh = 32; sh > 0; sh >>= 1)
+#pragma unroll
+                    for (int h = 0; h < G; ++h) ml[h] = __builtin_fmaxf(ml[h], __shfl_xor(ml[h], sh, 64));
+#pragma unroll
+                for (int h = 0; h < G; ++h) mcur[h] = ml[h];
+            }
         }
 #pragma unroll
         for (int u = 0; u < NVL; ++u) *reinterpret_cast<uint4*>(vw + 8 * (lane + 64 * u)) = vr[u];
@@ -689,12 +752,27 @@ hipError_t launch_fixed(const AttnArgs& a, int cus, hipStream_t stream) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attn_max_kernel, dim3((unsigned)((a.B * a.H + 255) / 256)), dim3(256), 0, stream, a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    // partials of head dims 128 and 256: one wave per item; when no wave has more than one
+    // item the waves take the row maxima themselves and the maximum kernel is not launched
+    // (measured 1-8 % faster with up to six query heads per kv head, 1 % slower with eight)
+    constexpr bool kInmax = (D == 128 || D == 256) && G < 8;
+    const int64_t gw = (items + 3) / 4 < 4 * (int64_t)cus ? (items + 3) / 4 : 4 * (int64_t)cus;
+    const bool inmax = kInmax && items <= 4 * gw;
+    if (!inmax) {
+        hipLaunchKernelGGL(attn_max_kernel, dim3((unsigned)((a.B * a.H + 255) / 256)), dim3(256), 0, stream, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     if constexpr (D == 128 || D == 256) {
-        const int64_t g3 = (items + 3) / 4 < 4 * (int64_t)cus ? (items + 3) / 4 : 4 * (int64_t)cus;
-        hipLaunchKernelGGL((attn_partials_wave_kernel<G, D>), dim3((unsigned)g3), dim3(256), 0, stream, a);
+        bool launched = false;
+        if constexpr (kInmax) {
+            if (inmax) {
+                hipLaunchKernelGGL((attn_partials_wave_kernel<G, D, true>), dim3((unsigned)gw), dim3(256), 0, stream, a);
+                launched = true;
+            }
+        }
+        if (!launched)
+            hipLaunchKernelGGL((attn_partials_wave_kernel<G, D, false>), dim3((unsigned)gw), dim3(256), 0, stream, a);
     } else {
         const int64_t lds3 = (int64_t)G * kAttnSeg * 4 + (int64_t)RS * (D + 8) * 2;
         const int64_t g3 = items < (kLdsPerCU / lds3) * cus ? items : (kLdsPerCU / lds3) * cus;

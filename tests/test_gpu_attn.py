@@ -166,3 +166,14 @@ def test_argument_errors():
     ws = torch.empty(8, dtype=torch.uint8, device=gu.dev())
     with pytest.raises(rg.RgError):                     # workspace too small
         rg.rg_attn_decode(q2, kc, kc.clone(), lens, torch.empty_like(q2), 1.0, workspace=ws)
+
+
+def test_both_row_maximum_paths():
+    """More work items than the partials kernel has waves (17 x 8 kv heads x 32 segments): the
+    row maxima come from the maximum kernel; the same sequences in a smaller batch take them
+    inside the partials kernel.  Both equal the oracle."""
+    B, H, Hkv, Lmax, D = 17, 32, 8, 8192, 128
+    lens = [8192 - 397 * b for b in range(B)]
+    q, kc, vc, got = _check(B, H, Hkv, Lmax, D, lens, seed=23)
+    got2 = _run(q[:3], kc[:3], vc[:3], lens[:3], np.float32(1.0 / np.sqrt(D)))
+    _assert_same(got2, got[:3], "first three sequences alone")
