@@ -364,11 +364,13 @@ __global__ void __launch_bounds__(256) attn_max_kernel(AttnArgs a) {
 // its NS steps take positions [l0 + s RS, l0 + s RS + RS) in turn (RS = 16384 / D
 // rows for the fixed head dims, else all 256 in one step), so every chain below
 // continues across the steps in ascending l.  e for the segment is computed at
-// its first step into LDS ([head][position], +0 past the sequence).  Unit u =
+// its first step into LDS ([head][position], -0 past the sequence).  Unit u =
 // (head, pair of adjacent d): two fmaf chains over the positions; threads tid < G
 // also run the segment sum of head tid (an addition chain).  Chains run over all
-// 256 positions of the segment: past the sequence e = +0 and the values are +0,
-// and adding +0 to a chain that starts at +0 and never becomes -0 changes no bit.
+// 256 positions of the segment: past the sequence e = -0 and the values are +0,
+// so a padded step is fmaf(-0, +0, n) = -0 + n = n and s + (-0) = s for every n and
+// s, including a numerator that is -0 (a negative product e * v that underflows).
+// (A +0 pad would turn such a -0 numerator into +0.)
 template <int G, int DM, int RS, bool EXACT>
 __global__ void __launch_bounds__(256) attn_partials_kernel(AttnArgs a) {
     constexpr int NS = kAttnSeg / RS;                 // steps per item
@@ -410,7 +412,7 @@ __global__ void __launch_bounds__(256) attn_partials_kernel(AttnArgs a) {
         tile.store(vs, RS, vpr, a.vmagic);
         if (st == 0) {
 #pragma unroll
-            for (int i = 0; i < G; ++i) es[i * kAttnSeg + tid] = tid < w.rows ? exp1(tr[i] - mr[i]) : 0.0f;
+            for (int i = 0; i < G; ++i) es[i * kAttnSeg + tid] = tid < w.rows ? exp1(tr[i] - mr[i]) : -0.0f;
         }
         __syncthreads();
         const Item cur = w;

@@ -45,6 +45,9 @@ struct WVec<uint16_t> {
     using V = uint4;
     static constexpr int E = 8;
     static __device__ __forceinline__ V zero() { return make_uint4(0u, 0u, 0u, 0u); }
+    static __device__ __forceinline__ V neg_zero() {   // every element bf16 -0 (0x8000)
+        return make_uint4(0x80008000u, 0x80008000u, 0x80008000u, 0x80008000u);
+    }
     static __device__ __forceinline__ float get(const V& v, int h) {
         const uint32_t d[4] = {v.x, v.y, v.z, v.w};
         return (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
@@ -55,6 +58,7 @@ struct WVec<float> {
     using V = float4;
     static constexpr int E = 4;
     static __device__ __forceinline__ V zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+    static __device__ __forceinline__ V neg_zero() { return make_float4(-0.f, -0.f, -0.f, -0.f); }
     static __device__ __forceinline__ float get(const V& v, int h) {
         const float d[4] = {v.x, v.y, v.z, v.w};
         return d[h];
@@ -784,8 +788,10 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
 // (first segment taken as is, later ones added in ascending order).
 //
 // Every slab runs all 16 steps: the missing k of a short last slab are
-// staged as +0 in x and W, and fmaf(+0, +0, p) = p for a chain that started
-// at +0 (such a chain is never -0), so the padded steps change no bit.
+// staged as +0 in x and -0 in W.  The product +0 * -0 is -0, and -0 + p = p
+// for every p (including p = -0, which a chain reaches when a negative
+// product underflows), so fmaf(+0, -0, p) = p and the padded steps change no
+// bit.  (A +0 weight would not do: fmaf(+0, +0, -0) = +0.)
 //
 // Occupancy.  One wave issues a VALU instruction only every few cycles on
 // gfx950 (measured with independent FMAs: ~51 TFLOP/s at one wave per SIMD,
@@ -833,7 +839,8 @@ __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT
     const int64_t m0 = (b / tiles_n) * BM, n0 = (b % tiles_n) * BN;
 
     // staging roles: x tile BM x 16 floats, W tile BN x 16 weights (16-byte vectors of WE);
-    // k >= K is staged as +0 (K % 8 == 0 on this path, so a vector is wholly in or out)
+    // k >= K is staged as x = +0, w = -0 (K % 8 == 0 on this path, so a vector is wholly
+    // in or out)
     using WV = WVec<WT>;
     constexpr int WE = WV::E, WPR = kTK / WE;        // weights per vector, vectors per tile row
     constexpr int XF4 = BM * kTK / 4 / 256;          // float4 loads per thread for x
@@ -856,7 +863,7 @@ __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT
             const int row = idx / WPR, kh = idx % WPR;
             const int64_t gn = n0 + row, gk = k0 + WE * kh;
             const bool ok = row < BN && gn < N && gk + WE <= K;
-            wr[u] = ok ? *reinterpret_cast<const typename WV::V*>(w + gn * K + gk) : WV::zero();
+            wr[u] = ok ? *reinterpret_cast<const typename WV::V*>(w + gn * K + gk) : WV::neg_zero();
         }
     };
     auto store_slab = [&](int buf) {

@@ -169,11 +169,23 @@ def test_argument_errors():
 
 
 def test_both_row_maximum_paths():
-    """More work items than the partials kernel has waves (17 x 8 kv heads x 32 segments): the
-    row maxima come from the maximum kernel; the same sequences in a smaller batch take them
-    inside the partials kernel.  Both equal the oracle."""
-    B, H, Hkv, Lmax, D = 17, 32, 8, 8192, 128
-    lens = [8192 - 397 * b for b in range(B)]
+    """More work items than the partials kernel has waves (16 per CU, so B x 8 kv heads x 32
+    segments with B = CUs / 16 + 1): the row maxima come from the maximum kernel; the same
+    sequences in a smaller batch take them inside the partials kernel.  Both equal the oracle."""
+    import paper_2609_25624_amd as rg
+    B = rg.rg_device_cu_count() // 16 + 1
+    H, Hkv, Lmax, D = 32, 8, 8192, 128
+    assert B * Hkv * (Lmax // 256) > 16 * rg.rg_device_cu_count()
+    lens = [8192 - 397 * (b % 17) for b in range(B)]
     q, kc, vc, got = _check(B, H, Hkv, Lmax, D, lens, seed=23)
     got2 = _run(q[:3], kc[:3], vc[:3], lens[:3], np.float32(1.0 / np.sqrt(D)))
     _assert_same(got2, got[:3], "first three sequences alone")
+
+
+@pytest.mark.parametrize("H,L", [(4, 33000), (3, 44000), (7, 19000)])
+def test_in_kernel_maximum_beyond_512_segment_maxima(H, L):
+    """One sequence long enough that its G x Jb segment maxima exceed the 512 a wave loads with
+    its first step (G = 4, 3, 7 query heads per kv head), so the partials wave folds the rest
+    in its tail loop.  One kv head: few work items, so the in-kernel maximum path is taken."""
+    assert H * (-(-L // 256)) > 512
+    _check(1, H, 1, L, 128, [L], seed=H * 7 + L)
