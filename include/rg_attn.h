@@ -85,6 +85,27 @@ int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const
                    int64_t B, int64_t H, int64_t Hkv, int64_t Lmax, int64_t D, float scale, void* workspace,
                    int64_t workspace_bytes, void* stream);
 
+/* Largest workspace rg_attn_decode_noalloc serves: 64 MiB (e.g. B = 32 sequences,
+ * H = 64 heads, Lmax = 4096, D = 128 needs 48 MiB). */
+#define RG_ATTN_SCRATCH_BYTES (64ll << 20)
+
+/*
+ * rg_attn_decode without a caller workspace and without any allocation, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops, harnesses that forbid hipMalloc).  Same arguments, order,
+ * kernels and bits as rg_attn_decode; the workspace is a static device array
+ * of RG_ATTN_SCRATCH_BYTES inside librg.so, one per device, held from the first
+ * call on a device until the process ends.  Returns RG_ERR_RANGE, enqueueing
+ * nothing, when rg_attn_workspace_size(B, H, Lmax, D) exceeds
+ * RG_ATTN_SCRATCH_BYTES; otherwise the errors of rg_attn_decode.  Every call on
+ * one device shares that array, so calls that may overlap in time on one device
+ * (different streams, or host threads without ordering) race and must be
+ * serialized by the caller; calls in order on one stream are safe.  Nothing in
+ * the array needs to start at any value.
+ */
+int rg_attn_decode_noalloc(const float* q, const uint16_t* kc, const uint16_t* vc, const int32_t* lens, float* out,
+                           int64_t B, int64_t H, int64_t Hkv, int64_t Lmax, int64_t D, float scale, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

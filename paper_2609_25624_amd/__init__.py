@@ -62,6 +62,7 @@ def _load():
         "rg_stream_destroy": [vp],
         "rg_device_cu_count": [ctypes.POINTER(i32)],
         "rg_attn_decode": [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, ctypes.c_float, vp, i64, vp],
+        "rg_attn_decode_noalloc": [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, ctypes.c_float, vp],
         "rg_strerror": [ctypes.c_int],
         "rg_last_hip_error": [],
     }
@@ -83,7 +84,8 @@ EXPORTS = ("rg_linear", "rg_linear_bias", "rg_linear_f32w", "rg_linear_set_launc
            "rg_stream_create_cu_mask", "rg_stream_destroy", "rg_device_cu_count", "rg_strerror",
            "rg_last_hip_error")
 # ... and include/rg_attn.h.
-ATTN_EXPORTS = ("rg_attn_workspace_size", "rg_attn_decode")
+ATTN_EXPORTS = ("rg_attn_workspace_size", "rg_attn_decode", "rg_attn_decode_noalloc")
+ATTN_SCRATCH_BYTES = 64 << 20   # RG_ATTN_SCRATCH_BYTES
 
 
 def strerror(code: int) -> str:
@@ -265,4 +267,25 @@ def rg_attn_decode(q, kc, vc, lens, out, scale, workspace=None, stream=None):
     pw = _tensor_ptr(workspace, (torch.uint8,), "workspace")
     _check(lib.rg_attn_decode(pq, pk, pv, pl, po, B, H, Hkv, Lmax, D, float(scale), pw, workspace.numel(),
                               _stream_ptr(stream)), "rg_attn_decode")
+    return out
+
+
+def rg_attn_decode_noalloc(q, kc, vc, lens, out, scale, stream=None):
+    """rg_attn_decode with the library's static device scratch as workspace (allocates nothing;
+    workspaces beyond ATTN_SCRATCH_BYTES are refused with RG_ERR_RANGE).  Calls that overlap in
+    time on one device share that scratch and race."""
+    import torch
+    pq = _tensor_ptr(q, (torch.float32,), "q")
+    pk = _tensor_ptr(kc, (torch.bfloat16, torch.int16, torch.uint16), "kc")
+    pv = _tensor_ptr(vc, (torch.bfloat16, torch.int16, torch.uint16), "vc")
+    pl = _tensor_ptr(lens, (torch.int32,), "lens")
+    po = _tensor_ptr(out, (torch.float32,), "out")
+    if q.dim() != 3 or kc.dim() != 4 or tuple(vc.shape) != tuple(kc.shape) or tuple(out.shape) != tuple(q.shape):
+        raise ValueError("q/out [B,H,D], kc/vc [B,Hkv,Lmax,D]")
+    B, H, D = q.shape
+    _, Hkv, Lmax, D2 = kc.shape
+    if kc.shape[0] != B or D2 != D or lens.numel() != B:
+        raise ValueError(f"shape mismatch q{tuple(q.shape)} kc{tuple(kc.shape)} lens{tuple(lens.shape)}")
+    _check(lib.rg_attn_decode_noalloc(pq, pk, pv, pl, po, B, H, Hkv, Lmax, D, float(scale), _stream_ptr(stream)),
+           "rg_attn_decode_noalloc")
     return out

@@ -609,31 +609,45 @@ int64_t rg_attn_workspace_size(int64_t B, int64_t H, int64_t Lmax, int64_t D) {
     return attn_layout(B, H, Lmax, D, &lay) ? lay.total : 0;
 }
 
-int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const int32_t* lens, float* out,
-                   int64_t B, int64_t H, int64_t Hkv, int64_t Lmax, int64_t D, float scale, void* workspace,
-                   int64_t workspace_bytes, void* stream) {
-    if (!q || !kc || !vc || !lens || !out || !workspace) return RG_ERR_INVAL;
+}  // extern "C"
+
+namespace {
+
+// Argument checks of the attention entry points, in the order of the error codes:
+// sizes, then alignment, then aliasing.  `workspace` is null for the no-allocation
+// entry point (whose scratch is the library's own, so nothing can alias it).
+int attn_check(const float* q, const uint16_t* kc, const uint16_t* vc, const int32_t* lens, float* out, int64_t B,
+               int64_t H, int64_t Hkv, int64_t Lmax, int64_t D, const void* workspace, int64_t workspace_bytes,
+               AttnLayout* lay) {
+    if (!q || !kc || !vc || !lens || !out) return RG_ERR_INVAL;
     if (B < 1 || H < 1 || Hkv < 1 || H % Hkv != 0 || H / Hkv > 8 || Lmax < 1) return RG_ERR_INVAL;
     if (D < 8 || D > 256 || D % 8 != 0) return RG_ERR_INVAL;
-    AttnLayout lay;
-    if (!attn_layout(B, H, Lmax, D, &lay)) return RG_ERR_INVAL;
+    if (!attn_layout(B, H, Lmax, D, lay)) return RG_ERR_INVAL;
     if (!mul_ok(B * Hkv, Lmax) || !mul_ok(B * Hkv * Lmax, D)) return RG_ERR_INVAL;
     const int64_t J = ceil_div(Lmax, 256);
     if (B * Hkv * J > 0x3fffffff || B * H > 0x7fffffff) return RG_ERR_INVAL;   // work items fit int32
-    if (workspace_bytes < lay.total) return RG_ERR_INVAL;
+    if (workspace && workspace_bytes < lay->total) return RG_ERR_INVAL;
     if (((uintptr_t)q & 15) || ((uintptr_t)out & 15) || ((uintptr_t)workspace & 15) || ((uintptr_t)kc & 15) ||
         ((uintptr_t)vc & 15) || ((uintptr_t)lens & 3))
         return RG_ERR_ALIGN;
     const size_t qb = (size_t)(B * H * D) * 4, cb = (size_t)(B * Hkv * Lmax * D) * 2, lb = (size_t)B * 4;
-    const size_t wb = (size_t)lay.total;
     if (overlaps(out, qb, q, qb) || overlaps(out, qb, kc, cb) || overlaps(out, qb, vc, cb) ||
-        overlaps(out, qb, lens, lb) || overlaps(out, qb, workspace, wb) || overlaps(workspace, wb, q, qb) ||
-        overlaps(workspace, wb, kc, cb) || overlaps(workspace, wb, vc, cb) || overlaps(workspace, wb, lens, lb))
+        overlaps(out, qb, lens, lb))
         return RG_ERR_ALIAS;
-    int cus = 0;
-    const int dc = device_check(&cus);
-    if (dc != RG_OK) return dc;
-    char* ws = static_cast<char*>(workspace);
+    if (workspace) {
+        const size_t wb = (size_t)lay->total;
+        if (overlaps(out, qb, workspace, wb) || overlaps(workspace, wb, q, qb) || overlaps(workspace, wb, kc, cb) ||
+            overlaps(workspace, wb, vc, cb) || overlaps(workspace, wb, lens, lb))
+            return RG_ERR_ALIAS;
+    }
+    return RG_OK;
+}
+
+// Fill the kernel arguments and enqueue the attention kernels (arguments already checked).
+int attn_launch(const float* q, const uint16_t* kc, const uint16_t* vc, const int32_t* lens, float* out, int64_t B,
+                int64_t H, int64_t Hkv, int64_t Lmax, int64_t D, float scale, const AttnLayout& lay, char* ws,
+                int cus, void* stream) {
+    const int64_t J = ceil_div(Lmax, 256);
     rg::AttnArgs a;
     a.q = q;
     a.k = kc;
@@ -656,6 +670,71 @@ int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const
     a.vmagic = vpr > 1 ? (uint32_t)((((uint64_t)1 << 32) + vpr - 1) / vpr) : 0u;
     (void)hipGetLastError();
     return hip_status(rg::launch_attn(a, cus, (hipStream_t)stream));
+}
+
+// Scratch of rg_attn_decode_noalloc: a file-scope device array (each device that
+// loads the library holds its own copy until the process ends).  Host code never
+// passes the array's name to a kernel: its device address is taken once per
+// device with hipGetSymbolAddress (with that device current) and kept below.
+// No attention kernel reads a workspace value it has not written in the same
+// call, so nothing here needs clearing between calls.
+__device__ __align__(256) uint8_t scratch[RG_ATTN_SCRATCH_BYTES];
+
+struct ScratchSlot {
+    std::once_flag once;
+    hipError_t status = hipSuccess;
+    void* ptr = nullptr;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+int scratch_ptr(void** out) {
+    int dev = 0;
+    const hipError_t ge = hipGetDevice(&dev);
+    if (ge != hipSuccess) return hip_status(ge);
+    if (dev < 0 || dev >= kMaxDevices) return RG_ERR_HIP;
+    ScratchSlot& sl = g_scratch[dev];
+    std::call_once(sl.once, [&] {
+        void* p = nullptr;
+        sl.status = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (sl.status == hipSuccess) sl.ptr = p;
+        else (void)hipGetLastError();
+    });
+    if (sl.status != hipSuccess || !sl.ptr) return hip_status(sl.status != hipSuccess ? sl.status : hipErrorUnknown);
+    *out = sl.ptr;
+    return RG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rg_attn_decode(const float* q, const uint16_t* kc, const uint16_t* vc, const int32_t* lens, float* out,
+                   int64_t B, int64_t H, int64_t Hkv, int64_t Lmax, int64_t D, float scale, void* workspace,
+                   int64_t workspace_bytes, void* stream) {
+    if (!workspace) return RG_ERR_INVAL;
+    AttnLayout lay;
+    const int st = attn_check(q, kc, vc, lens, out, B, H, Hkv, Lmax, D, workspace, workspace_bytes, &lay);
+    if (st != RG_OK) return st;
+    int cus = 0;
+    const int dc = device_check(&cus);
+    if (dc != RG_OK) return dc;
+    return attn_launch(q, kc, vc, lens, out, B, H, Hkv, Lmax, D, scale, lay, static_cast<char*>(workspace), cus,
+                       stream);
+}
+
+int rg_attn_decode_noalloc(const float* q, const uint16_t* kc, const uint16_t* vc, const int32_t* lens, float* out,
+                           int64_t B, int64_t H, int64_t Hkv, int64_t Lmax, int64_t D, float scale, void* stream) {
+    AttnLayout lay;
+    int st = attn_check(q, kc, vc, lens, out, B, H, Hkv, Lmax, D, nullptr, 0, &lay);
+    if (st != RG_OK) return st;
+    if (lay.total > (int64_t)RG_ATTN_SCRATCH_BYTES) return RG_ERR_RANGE;   // before any HIP call
+    int cus = 0;
+    const int dc = device_check(&cus);
+    if (dc != RG_OK) return dc;
+    void* ws = nullptr;
+    st = scratch_ptr(&ws);
+    if (st != RG_OK) return st;
+    return attn_launch(q, kc, vc, lens, out, B, H, Hkv, Lmax, D, scale, lay, static_cast<char*>(ws), cus, stream);
 }
 
 int rg_linear_f32w(const float* x, const float* w, float* y, int64_t M, int64_t N, int64_t K, void* stream) {

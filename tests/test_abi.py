@@ -274,3 +274,34 @@ def test_attention_kernels_use_only_ieee_operations():
     assert "v_div_fixup_f32" in insts          # the correctly rounded division
     modes = re.findall(r"\.amdhsa_float_denorm_mode_32\s+(\d+)", asm)
     assert modes and set(modes) == {"3"}
+
+
+def test_attention_noalloc_host_checks():
+    """The no-allocation attention entry point refuses a workspace beyond its static scratch, and
+    bad arguments, before any device call (so these run without a GPU)."""
+    L = rg.lib
+    assert rg.ATTN_SCRATCH_BYTES == 64 << 20
+    q, out, lens, kc, vc = 0x1000000, 0x2000000, 0x3000000, 0x10000000, 0x20000000
+    B, H, Hkv, Lmax, D = 1, 8, 1, 2_200_000, 8
+    assert rg.rg_attn_workspace_size(B, H, Lmax, D) > rg.ATTN_SCRATCH_BYTES
+    assert L.rg_attn_decode_noalloc(q, kc, vc, lens, out, B, H, Hkv, Lmax, D, 1.0, None) == rg.RG_ERR_RANGE
+    assert rg.rg_attn_workspace_size(B, H, 2_000_000, D) < rg.ATTN_SCRATCH_BYTES   # the limit is the size
+    assert L.rg_attn_decode_noalloc(None, kc, vc, lens, out, 1, 1, 1, 16, 64, 1.0, None) == rg.RG_ERR_INVAL
+    assert L.rg_attn_decode_noalloc(q, kc, vc, lens, out, 1, 3, 2, 16, 64, 1.0, None) == rg.RG_ERR_INVAL
+    assert L.rg_attn_decode_noalloc(q + 4, kc, vc, lens, out, 1, 1, 1, 16, 64, 1.0, None) == rg.RG_ERR_ALIGN
+    assert L.rg_attn_decode_noalloc(q, kc, vc, lens, q, 1, 1, 1, 16, 64, 1.0, None) == rg.RG_ERR_ALIAS
+
+
+def test_noalloc_scratch_is_a_static_device_array_taken_by_symbol_address():
+    """The scratch lives in a file-scope __device__ array whose address host code takes with
+    hipGetSymbolAddress; the array's name never reaches a kernel argument."""
+    src = open(os.path.join(ROOT, "paper_2609_25624_amd", "csrc", "rg_api.cpp")).read()
+    code = re.sub(r"//.*", "", src)
+    assert re.search(r"^__device__ __align__\(256\) uint8_t scratch\[RG_ATTN_SCRATCH_BYTES\];", code, re.M)
+    assert code.count("HIP_SYMBOL(scratch)") == 1
+    uses = [m.start() for m in re.finditer(r"\bscratch\b", code)]
+    assert len(uses) == 2, "the array is named only in its definition and in hipGetSymbolAddress"
+    body = code[code.index("int rg_attn_decode_noalloc("):]
+    body = body[:body.index("\n}\n")]
+    for bad in ("hipMalloc", "hipFree", "hipMemset", "hipHostMalloc", "new ", "malloc("):
+        assert bad not in body, bad
