@@ -172,13 +172,31 @@ def run_configs():
             vendor = dict(us_per_call=round(vus, 3), TFLOPs=round(flops / (vus * 1e-6) / 1e12, 3),
                           fused_over_vendor_time=round(us / vus, 3))
             del wt
+        argmax = None
+        if name == "lm_head":
+            # the greedy decision after the LM-head GEMV (lowest index among equal maxima), timed
+            # beside it: a separate launch that reads the logits back
+            idx = torch.empty(M, dtype=torch.int64, device=dev)
+            for i in range(3):
+                rg.rg_argmax_rows(y, idx, stream=stream)
+            torch.cuda.synchronize()
+            a.record(stream)
+            for i in range(R):
+                rg.rg_argmax_rows(y, idx, stream=stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            aus = a.elapsed_time(b) * 1e3 / R
+            want_idx = [oracle.argmax(got[m]) for m in range(M)]
+            argmax = dict(us_per_call=round(aus, 3), frac_of_gemv_time=round(aus / us, 4),
+                          logits_GBs=round(4.0 * M * N / (aus * 1e-6) / 1e9, 1),
+                          matches_oracle=idx.cpu().tolist() == want_idx)
         print(json.dumps({
             "config": cfg, "layer": name, "M": M, "N": N, "K": K, "us_per_call": round(us, 3),
             "weight_TBs": round(2.0 * N * K / (us * 1e-6) / 1e12, 4),
             "frac_of_8TBs": round(2.0 * N * K / (us * 1e-6) / (HBM_PEAK_GBS * 1e9), 4),
             "TFLOPs": round(tflops, 3), "frac_of_fp32_157": round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
             "bitexact": exact, "checked": checked, "kernel": plan["kernel_name"], "calls_timed": R,
-            "rotated_copies": nrot, "vendor_fp32_gemm": vendor}), flush=True)
+            "rotated_copies": nrot, "vendor_fp32_gemm": vendor, "argmax": argmax}), flush=True)
         del xd, ws, w0, y
         torch.cuda.empty_cache()
     run_variant_configs()
@@ -579,13 +597,13 @@ def main():
     # ---- the scheme the paper improves on: cast to an FP32 temporary, then FP32 GEMM ----
     scheme = None
     if not args.no_baseline_scheme:
+        from paper_2609_25624_amd import baseline as rgb
         tmp = {L["name"]: torch.empty((L["N"], L["K"]), dtype=torch.float32, device=dev) for L in layers}
 
         def scheme_step(i):
+            # the C-ABI comparison point: exact cast into the transient FP32 copy, then rocBLAS sgemm
             for L in layers:
-                wt = tmp[L["name"]]
-                rg.rg_cast_bf16_f32(L["ws"][i % len(L["ws"])], wt, stream=stream)
-                torch.matmul(L["xd"], wt.t(), out=L["y"])
+                rgb.rg_linear_cast_baseline(L["xd"], L["ws"][i % len(L["ws"])], tmp[L["name"]], L["y"], stream=stream)
 
         def gemm_step(i):
             for L in layers:
@@ -610,7 +628,8 @@ def main():
         scheme = dict(ms_per_step=round(sms, 4), gemm_only_ms_per_step=round(gms, 4),
                       speedup_of_fused=round(sms / ms_per_step, 3),
                       transient_fp32_bytes=int(max(4 * L["N"] * L["K"] for L in layers)),
-                      gemm="torch.matmul float32 (vendor BLAS); the GEMM-only figure reuses one FP32 copy")
+                      gemm="rg_linear_cast_baseline (exact cast, then rocBLAS sgemm); the GEMM-only figure is "
+                           "torch.matmul float32 on one resident FP32 copy")
         del tmp
 
     # ---- CPU oracle on the host: bounded sample of the same step ----
@@ -626,8 +645,22 @@ def main():
             el = time.perf_counter() - t_start
             if el >= args.cpu_seconds or reps >= 5000:
                 break
+        # the scalar definitional oracle on one thread, on a bounded sample of the same step
+        t_start = time.perf_counter()
+        reps1 = 0
+        while True:
+            for L in layers:
+                oracle.linear(L["x"], L["w"], nthreads=1)
+            reps1 += 1
+            el1 = time.perf_counter() - t_start
+            if el1 >= args.cpu_seconds / 2 or reps1 >= 5000:
+                break
         cpu = dict(value=round(reps * step_wbytes / el / 1e12, 6), unit="TB/s", cores=threads, kind="oracle",
-                   sample=f"{reps} full steps (4 layers, M=1) in {el:.1f} s")
+                   sample=f"{reps} full steps (4 layers, M=1) in {el:.1f} s",
+                   single_thread=dict(value=round(reps1 * step_wbytes / el1 / 1e12, 6), unit="TB/s", cores=1,
+                                      ms_per_step=round(el1 / reps1 * 1e3, 2),
+                                      sample=f"{reps1} full steps (4 layers, M=1) in {el1:.1f} s"),
+                   nproc=os.cpu_count(), cpu_model=_cpu_model())
 
     out = {
         "metric": METRIC,
@@ -653,6 +686,18 @@ def main():
         "baseline_scheme": scheme,
     }
     print(json.dumps(out), flush=True)
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def _layer_id(name):

@@ -46,6 +46,10 @@ def lib():
         L.rg_attn_oracle.restype = ci
         L.rg_oracle_argmax.argtypes = [vp, i64]
         L.rg_oracle_argmax.restype = i64
+        L.rg_oracle_fast_linear.argtypes = [vp, vp, vp, i64, i64, i64, ci]
+        L.rg_oracle_fast_linear.restype = ci
+        L.rg_oracle_fast_supported.argtypes = []
+        L.rg_oracle_fast_supported.restype = ci
         _lib = L
     return _lib
 
@@ -75,6 +79,27 @@ def linear(x, w, nthreads=None) -> np.ndarray:
     rc = lib().rg_oracle_linear(x.ctypes.data, w.ctypes.data, y.ctypes.data, M, N, K, _threads(nthreads))
     if rc != 0:
         raise ValueError("rg_oracle_linear rejected its arguments")
+    return y
+
+
+def fast_supported() -> bool:
+    """Whether this CPU runs the same-order vectorised oracle (AVX2 and FMA)."""
+    return bool(lib().rg_oracle_fast_supported())
+
+
+def linear_fast(x, w, nthreads=None) -> np.ndarray:
+    """linear() computed by the same-order vectorised oracle (rg_oracle_fast.c): the same operation
+    sequence per output, sixteen outputs per AVX2 register pair; bit-identical to linear() (pinned
+    by the tests).  For the largest workloads."""
+    x, w = _check(x, w)
+    M, K = x.shape
+    N = w.shape[0]
+    y = np.empty((M, N), dtype=np.float32)
+    rc = lib().rg_oracle_fast_linear(x.ctypes.data, w.ctypes.data, y.ctypes.data, M, N, K, _threads(nthreads))
+    if rc == -2:
+        raise RuntimeError("the same-order vectorised oracle needs AVX2 and FMA on the host CPU")
+    if rc != 0:
+        raise ValueError(f"rg_oracle_fast_linear failed ({rc})")
     return y
 
 

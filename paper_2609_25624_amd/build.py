@@ -23,6 +23,11 @@ NEGCTL_LIB = os.path.join(HERE, "librg_negctl.so")
 NEGCTL_SOURCES = ["rg_negctl.hip"]
 
 
+# The comparison point (cast, then the vendor FP32 GEMM): a library of its own, so that
+# librg.so has no BLAS dependency.  It calls librg's cast and rocBLAS.
+BASELINE_LIB = os.path.join(HERE, "librg_baseline.so")
+BASELINE_SOURCES = ["rg_baseline.cpp"]
+
 # A C program that uses the library through include/rg.h only (no Python).
 EXAMPLE_SRC = os.path.join(HERE, "examples", "linear_capi.c")
 EXAMPLE_BIN = os.path.join(HERE, "examples", "linear_capi")
@@ -31,6 +36,10 @@ EXAMPLE_BIN = os.path.join(HERE, "examples", "linear_capi")
 def build(verbose: bool = False) -> str:
     _build_lib(SOURCES, LIB, verbose)
     _build_lib(NEGCTL_SOURCES, NEGCTL_LIB, verbose)
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(HIPCC)))
+    _build_lib(BASELINE_SOURCES, BASELINE_LIB, verbose,
+               link=["-L" + HERE, "-lrg", "-L" + os.path.join(rocm, "lib"), "-lrocblas", "-Wl,-rpath,$ORIGIN",
+                     "-Wl,-rpath," + os.path.join(rocm, "lib")])
     _build_example(verbose)
     return LIB
 
@@ -49,7 +58,7 @@ def _build_example(verbose):
     os.replace(EXAMPLE_BIN + ".tmp", EXAMPLE_BIN)
 
 
-def _build_lib(sources, lib, verbose):
+def _build_lib(sources, lib, verbose, link=()):
     objs = []
     for src in sources:
         path = os.path.join(CSRC, src)
@@ -64,7 +73,7 @@ def _build_lib(sources, lib, verbose):
         if err.strip() and verbose:
             print(err)
         objs.append(obj)
-    cmd = [HIPCC, *DEVICE, "-shared", "-fPIC", *objs, "-o", lib + ".tmp"]
+    cmd = [HIPCC, *DEVICE, "-shared", "-fPIC", *objs, *link, "-o", lib + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -79,3 +79,25 @@ def sample_indices(M, N, count, seed=0):
 
 def log(msg):
     print(msg, flush=True)
+
+
+def stored_digest(case):
+    """The oracle-written full-output digest of a case of tests/golden/config_digests.json."""
+    import json
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "config_digests.json")
+    return json.load(open(path))["cases"][case]
+
+
+def assert_full_output(got, x, w, case):
+    """Every output of `got` against the stored oracle digest of `case`; on a mismatch the
+    oracle output is recomputed to name the first differing element."""
+    import hashlib
+    from tests.golden import make_config_digests as mk
+    c = stored_digest(case)
+    assert got.shape == (c["M"], c["N"]), (got.shape, case)
+    d = hashlib.sha256(np.ascontiguousarray(got, dtype=np.float32).tobytes()).hexdigest()[:16]
+    if d != c["sha256_16"]:
+        want = mk.oracle_output(dict(c, name=case), x, w)
+        assert_bitwise(got, want, f"{case} full output")
+        raise AssertionError(f"{case}: digest {d} != stored {c['sha256_16']} but the outputs match the oracle")

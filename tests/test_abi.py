@@ -305,3 +305,18 @@ def test_noalloc_scratch_is_a_static_device_array_taken_by_symbol_address():
     body = body[:body.index("\n}\n")]
     for bad in ("hipMalloc", "hipFree", "hipMemset", "hipHostMalloc", "new ", "malloc("):
         assert bad not in body, bad
+
+
+def test_baseline_library_exports_and_host_checks():
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "rg_baseline.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"^\s*int\s+(rg_\w+)\s*\(", text, flags=re.M)))
+    from paper_2609_25624_amd import baseline
+    assert sorted(baseline.EXPORTS) == names
+    L = baseline.lib
+    a, b, c, d = 0x1000000, 0x2000000, 0x3000000, 0x4000000
+    assert L.rg_linear_cast_baseline(None, b, c, d, 1, 1, 1, None) == rg.RG_ERR_INVAL
+    assert L.rg_linear_cast_baseline(a, b, c, d, 1, 0, 1, None) == rg.RG_ERR_INVAL
+    assert L.rg_linear_cast_baseline(a, b, c, d, 1, 1 << 31, 1, None) == rg.RG_ERR_INVAL
+    assert L.rg_linear_cast_baseline(a + 2, b, c, d, 1, 1, 1, None) == rg.RG_ERR_ALIGN
+    assert L.rg_linear_cast_baseline(a, b, a, d, 1, 1, 1, None) == rg.RG_ERR_ALIAS       # w_tmp over x
+    assert L.rg_linear_cast_baseline(a, b, c, c, 1, 1, 1, None) == rg.RG_ERR_ALIAS       # y over w_tmp

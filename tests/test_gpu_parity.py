@@ -77,18 +77,35 @@ def test_config3_batched_rows_equal_single_row(name, M):
 
 
 @pytest.mark.parametrize("name", list(L8B))
-def test_config3_m64_sampled(name):
+def test_config3_m64_full(name):
+    """Every output of the M = 64 batch against the oracle's stored full-output digest, a sample
+    against the definitional oracle computed here, and row 5 alone against row 5 in the batch."""
     import torch
+    import oracle
     N, K = L8B[name]
     x, w = gu.layer(64, N, K, layer_id=list(L8B).index(name))
     xd, wd = gu.to_dev(x, w)
     y = gu.run(xd, wd)
     torch.cuda.synchronize()
-    import oracle
+    got = y.cpu().numpy()
+    gu.assert_full_output(got, x, w, f"{name}_m64")
     rows, cols = gu.sample_indices(64, N, 3000)
-    gu.assert_bitwise(y.cpu().numpy()[rows, cols], oracle.linear_sampled(x, w, rows, cols), f"{name} M=64")
+    gu.assert_bitwise(got[rows, cols], oracle.linear_sampled(x, w, rows, cols), f"{name} M=64 sampled")
     y1 = gu.run(xd[5:6].contiguous(), wd)
-    gu.assert_bitwise(y1.cpu().numpy()[0], y.cpu().numpy()[5], f"{name} row 5 at M=64 vs M=1")
+    gu.assert_bitwise(y1.cpu().numpy()[0], got[5], f"{name} row 5 at M=64 vs M=1")
+
+
+@pytest.mark.parametrize("M", [4, 16])
+@pytest.mark.parametrize("name", list(L8B))
+def test_config3_full_output_digests(name, M):
+    import torch
+    N, K = L8B[name]
+    x64, w = gu.layer(64, N, K, layer_id=list(L8B).index(name))
+    x = np.ascontiguousarray(x64[:M])
+    xd, wd = gu.to_dev(x, w)
+    y = gu.run(xd, wd)
+    torch.cuda.synchronize()
+    gu.assert_full_output(y.cpu().numpy(), x, w, f"{name}_m{M}")
 
 
 def test_config4_lm_head_m1_and_m16():
@@ -101,6 +118,8 @@ def test_config4_lm_head_m1_and_m16():
     torch.cuda.synchronize()
     want1 = gu.oracle_full(x16[:1], w)
     gu.assert_bitwise(y1, want1, "lm_head M=1")
+    gu.assert_full_output(y1, x16[:1], w, "lm_head_m1")
+    gu.assert_full_output(y16, x16, w, "lm_head_m16")
     import oracle
     rows, cols = gu.sample_indices(16, N, 4000)
     gu.assert_bitwise(y16[rows, cols], oracle.linear_sampled(x16, w, rows, cols), "lm_head M=16 sampled")
@@ -157,14 +176,29 @@ def test_config4_near_tie_argmax(kstar, exact_tie):
 
 @pytest.mark.parametrize("name,N,K", [("70b_gate_up", 57344, 8192), ("70b_down", 8192, 28672)])
 def test_config5_70b_m1(name, N, K):
-    _check_layer(1, N, K, w_std=0.01, layer_id=9)
+    x, w, got = _check_layer(1, N, K, w_std=0.01, layer_id=9)
+    gu.assert_full_output(got, x, w, f"{name}_m1")
 
 
 @pytest.mark.parametrize("name,N,K", [("70b_gate_up", 57344, 8192), ("70b_down", 8192, 28672)])
-def test_config5_70b_m2048_sampled(name, N, K):
+def test_config5_70b_m2048_full(name, N, K):
+    """Every output of the 2048-row prefill layers against the oracle's stored full-output digest
+    (on a mismatch the same-order vectorised oracle names the first differing output), and a
+    sample against the definitional oracle computed here."""
+    import torch
+    import oracle
     import paper_2609_25624_amd as rg
     assert rg.rg_plan(2048, N, K)["kernel_name"] == "tiled"
-    _check_layer(2048, N, K, w_std=0.01, layer_id=9, sampled=4000)
+    gu.log(f"case 70B {name} M=2048")
+    x, w = gu.layer(2048, N, K, w_std=0.01, layer_id=9)
+    xd, wd = gu.to_dev(x, w)
+    y = gu.run(xd, wd)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy()
+    del xd, wd, y
+    gu.assert_full_output(got, x, w, f"{name}_m2048")
+    rows, cols = gu.sample_indices(2048, N, 4000)
+    gu.assert_bitwise(got[rows, cols], oracle.linear_sampled(x, w, rows, cols), f"{name} M=2048 sampled")
 
 
 @pytest.mark.parametrize("M,N,K", [(65, 130, 1000), (100, 1000, 1000), (128, 256, 4096), (129, 257, 264),
