@@ -11,6 +11,25 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "rg.h")
 
 
+_ASM_CACHE = {}
+
+
+def _device_asm(fname):
+    """gfx950 assembly of one of the library's sources, compiled once per test session."""
+    if fname not in _ASM_CACHE:
+        import subprocess
+        import tempfile
+        from paper_2609_25624_amd import build as b
+        src = os.path.join(ROOT, "paper_2609_25624_amd", "csrc", fname)
+        with tempfile.TemporaryDirectory() as d:
+            out = os.path.join(d, "k.s")
+            r = subprocess.run([b.HIPCC, "-x", "hip", *b.COMMON, *b.DEVICE, "--cuda-device-only", "-S", src, "-o", out],
+                               capture_output=True, text=True)
+            assert r.returncode == 0, r.stderr
+            _ASM_CACHE[fname] = open(out).read()
+    return _ASM_CACHE[fname]
+
+
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
@@ -159,16 +178,7 @@ def test_no_atomics_or_matrix_core_builtins_in_kernels():
 def test_device_code_uses_only_ieee_fma_for_accumulation():
     # Inspect the gfx950 assembly of our own kernels: no matrix-core, dot-product,
     # packed-FP32, mixed-precision or non-fused multiply-add instructions.
-    import subprocess
-    import tempfile
-    from paper_2609_25624_amd import build as b
-    src = os.path.join(ROOT, "paper_2609_25624_amd", "csrc", "rg_kernels.hip")
-    with tempfile.TemporaryDirectory() as d:
-        out = os.path.join(d, "k.s")
-        r = subprocess.run([b.HIPCC, "-x", "hip", *b.COMMON, *b.DEVICE, "--cuda-device-only", "-S", src, "-o", out],
-                           capture_output=True, text=True)
-        assert r.returncode == 0, r.stderr
-        asm = open(out).read()
+    asm = _device_asm("rg_kernels.hip")
     insts = re.findall(r"^\s+(v_[a-z0-9_]+)", asm, flags=re.M)
     assert insts
     for i in set(insts):
@@ -255,19 +265,11 @@ def test_attention_header_exports_and_host_checks():
 
 
 def test_attention_kernels_use_only_ieee_operations():
-    import subprocess
-    import tempfile
-    from paper_2609_25624_amd import build as b
     src = os.path.join(ROOT, "paper_2609_25624_amd", "csrc", "rg_attn.hip")
     code = re.sub(r"//.*", "", open(src).read())
     for bad in ("atomic", "mfma", "__expf", "__builtin_expf", "exp2f", "fast-math"):
         assert bad not in code, bad
-    with tempfile.TemporaryDirectory() as d:
-        out = os.path.join(d, "a.s")
-        r = subprocess.run([b.HIPCC, "-x", "hip", *b.COMMON, *b.DEVICE, "--cuda-device-only", "-S", src, "-o", out],
-                           capture_output=True, text=True)
-        assert r.returncode == 0, r.stderr
-        asm = open(out).read()
+    asm = _device_asm("rg_attn.hip")
     insts = set(re.findall(r"^\s+(v_[a-z0-9_]+)", asm, flags=re.M))
     for i in insts:
         assert not re.match(r"v_(mfma|dot\d|pk_(fma|mul|add)_f32|mad_f32|mac_f32|exp_f32|log_f32|fma_mix|mad_mix)", i), i
@@ -320,3 +322,17 @@ def test_baseline_library_exports_and_host_checks():
     assert L.rg_linear_cast_baseline(a + 2, b, c, d, 1, 1, 1, None) == rg.RG_ERR_ALIGN
     assert L.rg_linear_cast_baseline(a, b, a, d, 1, 1, 1, None) == rg.RG_ERR_ALIAS       # w_tmp over x
     assert L.rg_linear_cast_baseline(a, b, c, c, 1, 1, 1, None) == rg.RG_ERR_ALIAS       # y over w_tmp
+
+
+def test_inline_assembly_writes_no_register_asynchronously():
+    """A vector or scalar memory load issued from inline assembly writes its destination registers
+    when the data returns, which the compiler cannot see: it may copy or reuse those registers
+    before then (a build that loaded x this way reused a pending destination for a load address,
+    and faulted).  The only memory instruction the library's inline assembly may issue is the
+    global->LDS DMA (no register destination); every other asm instruction is synchronous."""
+    allowed = {"s_nop", "s_mov_b32", "global_load_lds_dwordx4", "s_waitcnt", "v_fmac_f32_dpp"}
+    for f in ("rg_kernels.hip", "rg_attn.hip"):
+        asm = _device_asm(f)
+        blocks = re.findall(r";;#ASMSTART\n(.*?);;#ASMEND", asm, flags=re.S)
+        ops = {ln.split()[0] for blk in blocks for ln in blk.splitlines() if ln.strip() and not ln.strip().startswith(";")}
+        assert ops <= allowed, (f, sorted(ops - allowed))
