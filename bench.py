@@ -57,6 +57,12 @@ def parse():
     ap.add_argument("--inst-summary", metavar="COUNTER_CSV",
                     help="summarise a rocprofv3 --pmc SQ_INSTS_VALU_FMA_F32 SQ_INSTS_MFMA SQ_INSTS_VALU_ADD_F32 "
                          "SQ_INSTS_VALU run of --profile-kernels (no GPU needed) and exit")
+    ap.add_argument("--profile-shape", metavar="M,N,K",
+                    help="short run for hardware counters: 20 launches of rg_linear at this shape (seeded inputs, "
+                         "three rotated weight copies), then exit")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("COUNTER_CSV", "M,N,K"),
+                    help="summarise a rocprofv3 --pmc CSV of a --profile-shape run: per-launch counter averages and "
+                         "derived issue rates (no GPU needed) and exit")
     ap.add_argument("--profile-kernels", action="store_true",
                     help="short run for hardware counters: 20 launches of the gate+up M=1 layer, then 5 plain "
                          "device copies of 256 MiB (the calibration kernel for HBM byte counters)")
@@ -90,6 +96,65 @@ def profile_kernels():
     torch.cuda.synchronize()
     print(json.dumps({"profiled": "gate_up decode x20, copy 256MiB x5", "copy_bytes": 256 << 20,
                       "decode_algorithmic_bytes": 2 * N * K + 4 * K + 4 * N}), flush=True)
+
+
+def profile_shape(M, N, K):
+    """Dispatches for rocprofv3 counter runs of one shape: 20 launches of rg_linear."""
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2609_25624_amd as rg
+    dev = torch.device("cuda:0")
+    x, w = synth.layer_inputs(M, N, K, seed=0, w_std=0.02, layer=2)
+    xd = torch.from_numpy(x).to(dev)
+    ws = [torch.from_numpy(w.view(np.int16)).to(dev)]
+    ws += [ws[0].clone() for _ in range(2)]
+    y = torch.empty((M, N), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    for i in range(20):
+        rg.rg_linear(xd, ws[i % 3], y)
+    torch.cuda.synchronize()
+    p = rg.rg_plan(M, N, K)
+    print(json.dumps({"profiled": f"rg_linear {M}x{N}x{K} x20", "kernel": p["kernel_name"],
+                      "waves_per_wg": p["waves_per_wg"], "grid_wgs": p["grid_wgs"], "tile_m": p["tile_m"],
+                      "tile_n": p["tile_n"], "depth": p["depth"]}), flush=True)
+
+
+def pmc_summary(path, shape):
+    """Per-launch averages of the counters in a rocprofv3 --pmc CSV of a --profile-shape run, with
+    the FMA instruction count the order implies (M*N*K/64 full-wave binary32 FMAs) and, when
+    GRBM_GUI_ACTIVE is present, issue rates per cycle per SIMD (256 CUs x 4 SIMDs)."""
+    M, N, K = [int(v) for v in shape.split(",")]
+    rows = [r for r in _csv_rows(path) if "rg::" in r["Kernel_Name"]]
+    names = sorted({r["Counter_Name"] for r in rows})
+    avg = {}
+    for c in names:
+        v = [float(r["Counter_Value"]) for r in rows if r["Counter_Name"] == c]
+        avg[c] = sum(v) / len(v)
+        print(f"{c}: {avg[c]:.0f} per launch over {len(v)} launches")
+    kern = sorted({r["Kernel_Name"].split("(")[0] for r in rows})
+    print(f"kernels: {', '.join(kern)}")
+    print(f"FMA wave instructions the order implies: M*N*K/64 = {M * N * K // 64}")
+    cyc = avg.get("GRBM_GUI_ACTIVE")
+    if cyc:
+        # GRBM_GUI_ACTIVE is summed over the 8 XCDs: cycles of one XCD = the sum / 8
+        xcd_cycles = cyc / 8
+        simds = 256 * 4
+        print(f"GPU-active cycles per launch (one XCD): {xcd_cycles:.0f}")
+        for c in ("SQ_INSTS_VALU_FMA_F32", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_INSTS_SALU", "SQ_INSTS_VMEM"):
+            if c in avg:
+                print(f"{c} per cycle per SIMD: {avg[c] / xcd_cycles / simds:.4f}")
+        if "SQ_INSTS_VALU_FMA_F32" in avg:
+            # a full-wave binary32 FMA occupies a SIMD for 2 cycles: at most 0.5 per cycle per SIMD
+            f = avg["SQ_INSTS_VALU_FMA_F32"] / xcd_cycles / simds / 0.5
+            print(f"FMA issue as a fraction of the 0.5 per cycle per SIMD limit: {f:.3f}")
+        if "SQ_LDS_BANK_CONFLICT" in avg and "SQ_ACTIVE_INST_LDS" in avg:
+            print(f"SQ_LDS_BANK_CONFLICT / SQ_ACTIVE_INST_LDS: {avg['SQ_LDS_BANK_CONFLICT'] / avg['SQ_ACTIVE_INST_LDS']:.3f}")
+        if "SQ_WAVE_CYCLES" in avg:
+            # SQ_*_CYCLES count in units of 4 cycles, summed over waves
+            print(f"resident waves per CU (SQ_WAVE_CYCLES x 4 / cycles / 256): {avg['SQ_WAVE_CYCLES'] * 4 / xcd_cycles / 256:.2f}")
+    print(f"kernel_source_hash = {_kernel_hash()}")
 
 
 CONFIGS = [
@@ -472,6 +537,9 @@ def main():
     if args.counter_summary:
         counter_summary(*args.counter_summary)
         return
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the library has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
@@ -490,6 +558,9 @@ def main():
     torch.backends.cuda.matmul.allow_tf32 = False
     if args.profile_kernels:
         profile_kernels()
+        return
+    if args.profile_shape:
+        profile_shape(*[int(v) for v in args.profile_shape.split(",")])
         return
     if args.configs:
         run_configs()
