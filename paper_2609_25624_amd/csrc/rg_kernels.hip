@@ -780,29 +780,32 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
 //
 // A 256-thread workgroup owns a BM x BN output tile (16 x 16 threads, each
 // holding TM x TN outputs, as two interleaved halves per dimension so that
-// LDS reads are conflict free).  K advances in slabs of 16: x[BM][16] and
-// up(W)[BN][16] are staged transposed in LDS (double buffered, the next slab
-// prefetched into registers while the current one is multiplied).  Each
-// output keeps two registers: the running chain of the current 256-wide
-// segment (from +0, ascending k) and the fold of the finished segments
-// (first segment taken as is, later ones added in ascending order).
+// LDS reads are conflict free).  K advances in slabs of KT (32 for the 128 x 128
+// two-waves-per-SIMD build, 16 otherwise): x[BM][KT] and up(W)[BN][KT] are
+// staged transposed in LDS (double buffered, the next slab prefetched into
+// registers while the current one is multiplied).  Each output keeps two
+// registers: the running chain of the current 256-wide segment (from +0,
+// ascending k) and the fold of the finished segments (first segment taken as
+// is, later ones added in ascending order).
 //
-// Every slab runs all 16 steps: the missing k of a short last slab are
+// Every slab runs all KT steps: the missing k of a short last slab are
 // staged as +0 in x and -0 in W.  The product +0 * -0 is -0, and -0 + p = p
 // for every p (including p = -0, which a chain reaches when a negative
 // product underflows), so fmaf(+0, -0, p) = p and the padded steps change no
 // bit.  (A +0 weight would not do: fmaf(+0, +0, -0) = +0.)
 //
-// Occupancy.  One wave issues a VALU instruction only every few cycles on
-// gfx950 (measured with independent FMAs: ~51 TFLOP/s at one wave per SIMD,
-// ~96 at two, ~125 at four), so the 128 x 128 tile comes in two builds:
-// two waves per SIMD with the next step's operands read ahead (204 registers,
-// no spills), and three waves per SIMD (at most 168 registers: one operand
-// set per step, a few registers spilled outside the FMA loop).  Per round of
-// resident workgroups the two are about equally fast; the planner takes the
-// three-wave build where its rounds of 3 workgroups per CU are clearly fuller.
+// Limits.  Each thread's 64 independent chains keep the FMA pipeline busy
+// (plain FMAs with 16 or more independent chains per wave measure ~69
+// TFLOP/s at one wave per SIMD and ~133 at two), so at two waves per SIMD the
+// limits are LDS (8 x 8 outputs read 1 byte per FMA, the same order as the
+// LDS return rate at the FMA peak) and the per-slab barrier, which the
+// 32-wide slab halves.  The 128 x 128 tile comes in two builds: two waves per
+// SIMD with the next step's operands read ahead (no spills), and three waves
+// per SIMD (at most 168 registers: one operand set per step, a few registers
+// spilled outside the FMA loop).  The planner takes the three-wave build only
+// where its rounds of 3 workgroups per CU are clearly fuller.
 // ---------------------------------------------------------------------------
-constexpr int kTK = 16;   // k per slab
+constexpr int kTK = 16;   // k per slab (the 128 x 128 two-waves-per-SIMD build: 32)
 
 // n consecutive floats from LDS (n = 2, 4 or 8; the address is n*4-byte aligned)
 template <int n>
@@ -820,8 +823,9 @@ __device__ __forceinline__ void lds_vec(const float* p, float* out) {
     }
 }
 
-// W3: the three-waves-per-SIMD build (one operand set per step).
-template <int BM, int BN, typename WT, bool W3>
+// KT: k per slab (a divisor of the segment length 256, so a slab never straddles a
+// segment); W3: the three-waves-per-SIMD build (one operand set per step).
+template <int BM, int BN, int KT, typename WT, bool W3>
 __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT* __restrict__ w,
                                            const float* __restrict__ bias, float* __restrict__ y, int64_t M,
                                            int64_t N, int64_t K, int reverse) {
@@ -829,8 +833,9 @@ __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT
     constexpr int HM = TM / 2, HN = TN / 2;          // two interleaved halves
     static_assert(TM % 2 == 0 && TN % 2 == 0, "tile");
     constexpr int PADM = BM + 4, PADN = BN + 4;
-    __shared__ __attribute__((aligned(16))) float xs[2][kTK][PADM];
-    __shared__ __attribute__((aligned(16))) float ws[2][kTK][PADN];
+    static_assert(kChunk % KT == 0, "slabs inside segments");
+    __shared__ __attribute__((aligned(16))) float xs[2][KT][PADM];
+    __shared__ __attribute__((aligned(16))) float ws[2][KT][PADN];
 
     const int tid = threadIdx.x;
     const int tn = tid & 15, tm = tid >> 4;
@@ -842,8 +847,8 @@ __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT
     // k >= K is staged as x = +0, w = -0 (K % 8 == 0 on this path, so a vector is wholly
     // in or out)
     using WV = WVec<WT>;
-    constexpr int WE = WV::E, WPR = kTK / WE;        // weights per vector, vectors per tile row
-    constexpr int XF4 = BM * kTK / 4 / 256;          // float4 loads per thread for x
+    constexpr int WE = WV::E, WPR = KT / WE;         // weights per vector, vectors per tile row
+    constexpr int XF4 = BM * KT / 4 / 256;           // float4 loads per thread for x
     constexpr int WU4 = (BN * WPR + 255) / 256;      // weight vector loads per thread
     float4 xr[XF4];
     typename WV::V wr[WU4];
@@ -851,8 +856,8 @@ __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT
     auto load_slab = [&](int64_t k0) {
 #pragma unroll
         for (int u = 0; u < XF4; ++u) {
-            const int idx = tid + 256 * u;            // over BM rows x 4 float4
-            const int row = idx >> 2, kq = idx & 3;
+            const int idx = tid + 256 * u;            // over BM rows x KT/4 float4
+            const int row = idx / (KT / 4), kq = idx % (KT / 4);
             const int64_t gm = m0 + row, gk = k0 + 4 * kq;
             const bool ok = gm < M && gk + 4 <= K;
             xr[u] = ok ? *reinterpret_cast<const float4*>(x + gm * K + gk) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -870,7 +875,7 @@ __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT
 #pragma unroll
         for (int u = 0; u < XF4; ++u) {
             const int idx = tid + 256 * u;
-            const int row = idx >> 2, kq = idx & 3;
+            const int row = idx / (KT / 4), kq = idx % (KT / 4);
             xs[buf][4 * kq + 0][row] = xr[u].x;
             xs[buf][4 * kq + 1][row] = xr[u].y;
             xs[buf][4 * kq + 2][row] = xr[u].z;
@@ -893,18 +898,18 @@ __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = 0.0f, tot[i][j] = 0.0f;
 
-    const int64_t nslabs = (K + kTK - 1) / kTK;
+    const int64_t nslabs = (K + KT - 1) / KT;
     load_slab(0);
     store_slab(0);
     __syncthreads();
     for (int64_t sl = 0; sl < nslabs; ++sl) {
         const int buf = (int)(sl & 1);
-        if (sl + 1 < nslabs) load_slab((sl + 1) * kTK);
+        if (sl + 1 < nslabs) load_slab((sl + 1) * KT);
         if constexpr (W3) {
             // one operand set per step; the scheduling barrier keeps later steps' reads from
             // being hoisted into registers (three waves per SIMD hide the LDS latency instead)
 #pragma unroll
-            for (int kk = 0; kk < kTK; ++kk) {
+            for (int kk = 0; kk < KT; ++kk) {
                 float xv[TM], wv[TN];
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
@@ -929,9 +934,9 @@ __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT
             };
             read_k(0, 0);
 #pragma unroll
-            for (int kk = 0; kk < kTK; ++kk) {
+            for (int kk = 0; kk < KT; ++kk) {
                 const int r = kk & 1;
-                if (kk + 1 < kTK) read_k(kk + 1, r ^ 1);
+                if (kk + 1 < KT) read_k(kk + 1, r ^ 1);
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -939,7 +944,7 @@ __device__ __forceinline__ void tiled_body(const float* __restrict__ x, const WT
             }
         }
         // end of a 256-wide segment (or of K): fold the segment chain, restart it from +0
-        const int64_t kend = min((sl + 1) * kTK, K);
+        const int64_t kend = min((sl + 1) * KT, K);
         if ((kend % kChunk) == 0 || kend == K) {
             const bool first = kend <= kChunk;
 #pragma unroll
@@ -971,7 +976,8 @@ template <int BM, int BN, typename WT>
 __global__ void __launch_bounds__(256) tiled_kernel(const float* __restrict__ x, const WT* __restrict__ w,
                                                     const float* __restrict__ bias, float* __restrict__ y, int64_t M,
                                                     int64_t N, int64_t K, int reverse) {
-    tiled_body<BM, BN, WT, false>(x, w, bias, y, M, N, K, reverse);
+    // 32 k per slab for the 128 x 128 tile (half the barriers; measured 4-12 % faster), 16 otherwise
+    tiled_body<BM, BN, (BM == 128 && BN == 128) ? 32 : kTK, WT, false>(x, w, bias, y, M, N, K, reverse);
 }
 
 // The 128 x 128 tile built for three waves per SIMD.
@@ -979,7 +985,7 @@ template <typename WT>
 __global__ void __launch_bounds__(256, 3) tiled3_kernel(const float* __restrict__ x, const WT* __restrict__ w,
                                                        const float* __restrict__ bias, float* __restrict__ y,
                                                        int64_t M, int64_t N, int64_t K, int reverse) {
-    tiled_body<128, 128, WT, true>(x, w, bias, y, M, N, K, reverse);
+    tiled_body<128, 128, kTK, WT, true>(x, w, bias, y, M, N, K, reverse);
 }
 
 // ---------------------------------------------------------------------------
