@@ -92,7 +92,8 @@ typedef enum {
  *                   or 4 when K > 4096; ktile: 4, or 8 with tile_n 16)
  *   grid_wgs      : 1..65536 workgroups (work is spread over them evenly)
  *   depth         : 2..3  decode pipeline depth in 128-byte-per-row slabs (unused by gemv);
- *                   tiled kernel with 128 x 128 tiles: the build for 2 or 3 waves per SIMD
+ *                   tiled kernel with 128 x 128 tiles: the build for 2 or 3 waves per SIMD;
+ *                   ktile: 2 = 4 x 4, 3 = 4 x 8 outputs per thread (tile_n 32 or 64 only)
  *   grid_order    : 0 = forward, 1 = reversed workgroup-to-rows mapping
  *   tile_n        : 0 = planner default, else 16, 32 or 64: ktile's W rows per tile
  *   reserved      : must be 0
@@ -115,7 +116,8 @@ typedef struct {
     int32_t kernel;        /* rg_kernel_id */
     int32_t waves_per_wg;
     int32_t grid_wgs;
-    int32_t depth;         /* decode: pipeline depth; tiled 128 x 128: waves per SIMD (2 or 3) */
+    int32_t depth;         /* decode: pipeline depth; tiled 128 x 128: waves per SIMD (2 or 3);
+                              ktile: 2 = 4 x 4, 3 = 4 x 8 outputs per thread */
     int32_t rows_per_round;/* decode: W rows per workgroup round */
     int32_t tile_m, tile_n;/* tiled: output tile */
 } rg_plan_t;

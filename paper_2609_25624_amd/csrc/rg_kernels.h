@@ -66,9 +66,9 @@ hipError_t launch_tiled(const float* x, const uint16_t* w, const float* bias, fl
 hipError_t launch_tiled(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
                         int bm, int bn, int occ, int reverse, hipStream_t stream);
 hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int nt, int reverse, hipStream_t stream);
+                        int bm, int bn, int nt, int cn, int reverse, hipStream_t stream);
 hipError_t launch_ktile(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int nt, int reverse, hipStream_t stream);
+                        int bm, int bn, int nt, int cn, int reverse, hipStream_t stream);
 // Fixed-order decode attention (include/rg_attn.h).  The workspace regions are
 // carved by the caller: t [B][H][Lmax], segmax and spart [B][H][J], mmax [B][H],
 // npart [B][H][J][D].  `cus`: compute units of the device (sizes the persistent grids).

@@ -1003,11 +1003,12 @@ __global__ void __launch_bounds__(256, 3) tiled3_kernel(const float* __restrict_
 // sum).  Splitting K this way gives small-M shapes enough independent work
 // for several waves per SIMD while the order stays the documented one.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int KS, int NT, typename WT>
+template <int BM, int BN, int KS, int NT, typename WT, int CN>
 __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, const WT* __restrict__ w,
                                                    const float* __restrict__ bias, float* __restrict__ y, int64_t M, int64_t N, int64_t K,
                                                    int reverse) {
-    static_assert(BM * BN * KS == 16 * NT, "NT threads x 16 outputs");
+    static_assert(CN == 4 || CN == 8, "W rows per thread");
+    static_assert(BM * BN * KS == 4 * CN * NT, "NT threads x 4 CN outputs");
     constexpr int TG = NT / KS;                      // threads per group
     constexpr int KT = KS >= 8 ? 8 : 16;             // elements per slab
     constexpr int NSL = kChunk / KT;                 // slabs per segment
@@ -1018,7 +1019,7 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
     constexpr int WPT = (BN * WPR + TG - 1) / TG;    // weight vector loads per thread
     __shared__ __attribute__((aligned(16))) float xs[KS][2][KT][PADM];
     __shared__ __attribute__((aligned(16))) float ws[KS][2][KT][PADN];
-    __shared__ __attribute__((aligned(16))) float part[KS > 1 ? KS - 1 : 1][TG][16];
+    __shared__ __attribute__((aligned(16))) float part[KS > 1 ? KS - 1 : 1][TG][4 * CN];
 
     const int tid = threadIdx.x;
     const int g = tid / TG, tg = tid % TG;
@@ -1075,9 +1076,9 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
         }
     };
 
-    float acc[16], tot[16];
+    float acc[4 * CN], tot[4 * CN];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) tot[i] = 0.0f;
+    for (int i = 0; i < 4 * CN; ++i) tot[i] = 0.0f;
 
     load_slab(0, 0);
     store_slab(0);
@@ -1087,7 +1088,7 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
         const int64_t j = (int64_t)t * KS + g;
         const int len = j < J ? (int)min((int64_t)kChunk, K - j * kChunk) : 0;   // this group's segment length
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+        for (int i = 0; i < 4 * CN; ++i) acc[i] = 0.0f;
         for (int sl = 0; sl < NSL; ++sl) {
             const bool more = sl + 1 < NSL || t + 1 < rounds;
             if (more) load_slab(sl + 1 < NSL ? t : t + 1, sl + 1 < NSL ? sl + 1 : 0);
@@ -1096,22 +1097,32 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
 #pragma unroll
                 for (int kk = 0; kk < KT; ++kk) {
                     const float4 xv = *reinterpret_cast<const float4*>(&xs[g][buf][kk][4 * mi]);
-                    const float4 wv = *reinterpret_cast<const float4*>(&ws[g][buf][kk][4 * ni]);
-                    const float xa[4] = {xv.x, xv.y, xv.z, xv.w}, wa[4] = {wv.x, wv.y, wv.z, wv.w};
+                    const float xa[4] = {xv.x, xv.y, xv.z, xv.w};
+                    float wa[CN];
+#pragma unroll
+                    for (int q = 0; q < CN; q += 4) {
+                        const float4 wv = *reinterpret_cast<const float4*>(&ws[g][buf][kk][CN * ni + q]);
+                        wa[q] = wv.x; wa[q + 1] = wv.y; wa[q + 2] = wv.z; wa[q + 3] = wv.w;
+                    }
 #pragma unroll
                     for (int r = 0; r < 4; ++r)
 #pragma unroll
-                        for (int c = 0; c < 4; ++c) acc[4 * r + c] = __builtin_fmaf(xa[r], wa[c], acc[4 * r + c]);
+                        for (int c = 0; c < CN; ++c) acc[CN * r + c] = __builtin_fmaf(xa[r], wa[c], acc[CN * r + c]);
                 }
             } else {
                 for (int kk = 0; kk < kvalid; ++kk) {
                     const float4 xv = *reinterpret_cast<const float4*>(&xs[g][buf][kk][4 * mi]);
-                    const float4 wv = *reinterpret_cast<const float4*>(&ws[g][buf][kk][4 * ni]);
-                    const float xa[4] = {xv.x, xv.y, xv.z, xv.w}, wa[4] = {wv.x, wv.y, wv.z, wv.w};
+                    const float xa[4] = {xv.x, xv.y, xv.z, xv.w};
+                    float wa[CN];
+#pragma unroll
+                    for (int q = 0; q < CN; q += 4) {
+                        const float4 wv = *reinterpret_cast<const float4*>(&ws[g][buf][kk][CN * ni + q]);
+                        wa[q] = wv.x; wa[q + 1] = wv.y; wa[q + 2] = wv.z; wa[q + 3] = wv.w;
+                    }
 #pragma unroll
                     for (int r = 0; r < 4; ++r)
 #pragma unroll
-                        for (int c = 0; c < 4; ++c) acc[4 * r + c] = __builtin_fmaf(xa[r], wa[c], acc[4 * r + c]);
+                        for (int c = 0; c < CN; ++c) acc[CN * r + c] = __builtin_fmaf(xa[r], wa[c], acc[CN * r + c]);
                 }
             }
             if (more) {
@@ -1124,19 +1135,19 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
         if constexpr (KS > 1) {
             if (g > 0) {
 #pragma unroll
-                for (int i = 0; i < 16; i += 4)
+                for (int i = 0; i < 4 * CN; i += 4)
                     *reinterpret_cast<float4*>(&part[g - 1][tg][i]) = make_float4(acc[i], acc[i + 1], acc[i + 2], acc[i + 3]);
             }
             __syncthreads();
         }
         if (g == 0) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) tot[i] = (t == 0) ? acc[i] : tot[i] + acc[i];
+            for (int i = 0; i < 4 * CN; ++i) tot[i] = (t == 0) ? acc[i] : tot[i] + acc[i];
             if constexpr (KS > 1) {
                 for (int gg = 1; gg < KS; ++gg) {
                     if ((int64_t)t * KS + gg >= J) break;
 #pragma unroll
-                    for (int i = 0; i < 16; i += 4) {
+                    for (int i = 0; i < 4 * CN; i += 4) {
                         const float4 pv = *reinterpret_cast<const float4*>(&part[gg - 1][tg][i]);
                         tot[i] = tot[i] + pv.x;
                         tot[i + 1] = tot[i + 1] + pv.y;
@@ -1155,9 +1166,9 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
             const int64_t gm = m0 + 4 * mi + r;
             if (gm >= M) continue;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const int64_t gn = n0 + 4 * ni + c;
-                if (gn < N) y[gm * N + gn] = bias ? tot[4 * r + c] + bias[gn] : tot[4 * r + c];
+            for (int c = 0; c < CN; ++c) {
+                const int64_t gn = n0 + CN * ni + c;
+                if (gn < N) y[gm * N + gn] = bias ? tot[CN * r + c] + bias[gn] : tot[CN * r + c];
             }
         }
     }
@@ -1801,31 +1812,33 @@ hipError_t launch_tiled(const float* x, const float* w, const float* bias, float
 // Small-M tiles (16 outputs per thread, K shared out over KS = 16 * nt / (bm * bn) groups).
 template <typename WT>
 static hipError_t launch_ktile_t(const float* x, const WT* w, const float* bias, float* y, int64_t M, int64_t N,
-                                 int64_t K, int bm, int bn, int nt, int reverse, hipStream_t stream) {
+                                 int64_t K, int bm, int bn, int nt, int cn, int reverse, hipStream_t stream) {
     const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     if (tiles > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid((unsigned)tiles);
-#define RG_KT(BM, BN, NT) \
-    if (bm == BM && bn == BN && nt == NT) { \
-        hipLaunchKernelGGL((ktile_kernel<BM, BN, 16 * NT / (BM * BN), NT, WT>), grid, dim3(NT), 0, stream, x, w, bias, y, M, \
-                           N, K, reverse); \
+#define RG_KT(BM, BN, NT, CN) \
+    if (bm == BM && bn == BN && nt == NT && cn == CN) { \
+        hipLaunchKernelGGL((ktile_kernel<BM, BN, 4 * CN * NT / (BM * BN), NT, WT, CN>), grid, dim3(NT), 0, stream, x, w, bias, \
+                           y, M, N, K, reverse); \
         return hipGetLastError(); \
     }
-    RG_KT(16, 16, 256) RG_KT(16, 32, 256) RG_KT(16, 64, 256) RG_KT(32, 16, 256) RG_KT(32, 32, 256) RG_KT(32, 64, 256)
-    RG_KT(64, 16, 256) RG_KT(64, 32, 256) RG_KT(64, 64, 256)
-    RG_KT(16, 16, 512) RG_KT(32, 16, 512) RG_KT(64, 16, 512)
+    RG_KT(16, 16, 256, 4) RG_KT(16, 32, 256, 4) RG_KT(16, 64, 256, 4) RG_KT(32, 16, 256, 4) RG_KT(32, 32, 256, 4)
+    RG_KT(32, 64, 256, 4) RG_KT(64, 16, 256, 4) RG_KT(64, 32, 256, 4) RG_KT(64, 64, 256, 4)
+    RG_KT(16, 16, 512, 4) RG_KT(32, 16, 512, 4) RG_KT(64, 16, 512, 4)
+    RG_KT(16, 32, 256, 8) RG_KT(16, 64, 256, 8) RG_KT(32, 32, 256, 8) RG_KT(32, 64, 256, 8) RG_KT(64, 32, 256, 8)
+    RG_KT(64, 64, 256, 8)
 #undef RG_KT
     return hipErrorInvalidValue;
 }
 
 hipError_t launch_ktile(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int nt, int reverse, hipStream_t stream) {
-    return launch_ktile_t(x, w, bias, y, M, N, K, bm, bn, nt, reverse, stream);
+                        int bm, int bn, int nt, int cn, int reverse, hipStream_t stream) {
+    return launch_ktile_t(x, w, bias, y, M, N, K, bm, bn, nt, cn, reverse, stream);
 }
 
 hipError_t launch_ktile(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
-                        int bm, int bn, int nt, int reverse, hipStream_t stream) {
-    return launch_ktile_t(x, w, bias, y, M, N, K, bm, bn, nt, reverse, stream);
+                        int bm, int bn, int nt, int cn, int reverse, hipStream_t stream) {
+    return launch_ktile_t(x, w, bias, y, M, N, K, bm, bn, nt, cn, reverse, stream);
 }
 
 template <typename WT>

@@ -288,13 +288,15 @@ def test_round_major_quad_placement(M, kernel, N, K, grid, order):
 
 @pytest.mark.parametrize("M", [2, 5, 9, 16, 17, 33, 64, 100])
 @pytest.mark.parametrize("N,K", [(3, 4096), (1030, 4104), (301, 8192), (130, 14336), (77, 520)])
-@pytest.mark.parametrize("tile_n,waves", [(0, 0), (16, 4), (16, 8), (32, 0), (64, 0)])
-def test_ktile_shapes(M, N, K, tile_n, waves):
+@pytest.mark.parametrize("tile_n,waves,depth", [(0, 0, 0), (16, 4, 0), (16, 8, 0), (32, 0, 0), (64, 0, 0),
+                                                (32, 0, 3), (64, 0, 3)])
+def test_ktile_shapes(M, N, K, tile_n, waves, depth):
     """Small-M tiles with K shared out over thread groups: partial tiles in M and N, a short
     last segment (K % 256 != 0), rounds where only some groups have a segment (J % KS != 0),
-    every tile width, and (forced) more than one tile of rows."""
+    every tile width, 4 x 4 and 4 x 8 register tiles per thread (depth 3), and (forced) more
+    than one tile of rows."""
     import paper_2609_25624_amd as rg
-    rg.rg_linear_set_launch(kernel="ktile", tile_n=tile_n, waves_per_wg=waves)
+    rg.rg_linear_set_launch(kernel="ktile", tile_n=tile_n, waves_per_wg=waves, depth=depth)
     try:
         assert rg.rg_plan(M, N, K)["kernel_name"] == "ktile"
         _check_layer(M, N, K, seed=M * 7 + N + K)
@@ -414,6 +416,8 @@ def _launch_settings():
         dict(kernel="ktile", tile_n=32),
         dict(kernel="ktile", tile_n=64, grid_order=1),
         dict(kernel="ktile", tile_n=16, waves_per_wg=8),
+        dict(kernel="ktile", tile_n=32, depth=3),
+        dict(kernel="ktile", tile_n=64, depth=3, grid_order=1),
         dict(kernel="stream"),
         dict(kernel="stream", grid_wgs=7, grid_order=1),
     ]
