@@ -63,6 +63,13 @@ def parse():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("COUNTER_CSV", "M,N,K"),
                     help="summarise a rocprofv3 --pmc CSV of a --profile-shape run: per-launch counter averages and "
                          "derived issue rates (no GPU needed) and exit")
+    ap.add_argument("--group-trace", metavar="KERNEL_TRACE_CSV",
+                    help="group the library's dispatches in a rocprofv3 --kernel-trace CSV by kernel instance and "
+                         "launch shape (workgroups, workgroup size, LDS, VGPRs, scratch) in order of first dispatch, "
+                         "with calls and average/minimum duration (no GPU needed) and exit")
+    ap.add_argument("--floors", action="store_true",
+                    help="read floors of the M=1 Llama-3-8B layers: librg_probe's read kernel over exactly the "
+                         "layer's weight bytes, cold (the same rotation as the benchmark), one JSON line each")
     ap.add_argument("--profile-kernels", action="store_true",
                     help="short run for hardware counters: 20 launches of the gate+up M=1 layer, then 5 plain "
                          "device copies of 256 MiB (the calibration kernel for HBM byte counters)")
@@ -96,6 +103,60 @@ def profile_kernels():
     torch.cuda.synchronize()
     print(json.dumps({"profiled": "gate_up decode x20, copy 256MiB x5", "copy_bytes": 256 << 20,
                       "decode_algorithmic_bytes": 2 * N * K + 4 * K + 4 * N}), flush=True)
+
+
+def run_floors():
+    """Read floors of the M=1 Llama-3-8B layers: librg_probe's read kernel (every wave reading whole
+    8 KB pieces, adjacent across the grid, no arithmetic) over exactly the layer's weight bytes, cold
+    (the benchmark's rotated copies), at the best of several grid sizes, beside rg_linear on the same
+    copies.  Median of 5 loops of 200 calls each."""
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2609_25624_amd as rg
+    from paper_2609_25624_amd import probe
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    for li, (name, N, K) in enumerate(LAYERS):
+        x, w = synth.layer_inputs(1, N, K, seed=0, w_std=0.02, layer=li)
+        xd = torch.from_numpy(x).to(dev)
+        w0 = torch.from_numpy(w.view(np.int16)).to(dev)
+        nrot = max(1, int(np.ceil(ROTATE_BYTES / (2.0 * N * K))))
+        ws = [w0] + [w0.clone() for _ in range(nrot - 1)]
+        y = torch.empty((1, N), dtype=torch.float32, device=dev)
+        sink = torch.empty(4096 * 256, dtype=torch.int32, device=dev)
+
+        def timed(fn, R=200):
+            for i in range(10):
+                fn(i)
+            torch.cuda.synchronize()
+            loops = []
+            for rep in range(5):
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for i in range(R):
+                    fn(i)
+                b.record(stream)
+                torch.cuda.synchronize()
+                loops.append(a.elapsed_time(b) * 1e3 / R)
+            return sorted(loops)[2]
+
+        floors = {g: timed(lambda i, g=g: probe.rg_probe_read(ws[i % nrot], sink, g, stream=stream))
+                  for g in (256, 512, 1024, 2048, 4096)}
+        g_best = min(floors, key=floors.get)
+        lin_us = timed(lambda i: rg.rg_linear(xd, ws[i % nrot], y, stream=stream))
+        wb = 2.0 * N * K
+        print(json.dumps({"layer": name, "N": N, "K": K, "weight_bytes": int(wb),
+                          "read_floor_us": round(floors[g_best], 3),
+                          "read_floor_TBs": round(wb / (floors[g_best] * 1e-6) / 1e12, 4), "floor_grid": g_best,
+                          "floor_us_by_grid": {str(g): round(v, 3) for g, v in floors.items()},
+                          "rg_linear_us": round(lin_us, 3), "rg_linear_TBs": round(wb / (lin_us * 1e-6) / 1e12, 4),
+                          "rg_linear_over_floor_time": round(lin_us / floors[g_best], 3), "rotated_copies": nrot}),
+              flush=True)
+        del ws, w0, xd, y, sink
+        torch.cuda.empty_cache()
 
 
 def profile_shape(M, N, K):
@@ -463,6 +524,24 @@ def attn_trace_summary(path):
               f"{tot:8.2f} {kvb / (tot * 1e-6) / 1e12:8.3f}")
 
 
+def group_trace(path):
+    """The library's dispatches (rg:: kernels) grouped by kernel instance and launch shape."""
+    groups = {}
+    for r in _csv_rows(path):
+        name = r["Kernel_Name"]
+        if "rg::" not in name:
+            continue
+        short = re.sub(r"\(.*", "", name.replace("void ", "").replace("rg::", "").replace("(anonymous namespace)::", ""))
+        short = short.replace("unsigned short", "bf16")
+        wg = int(r["Workgroup_Size_X"])
+        key = (short, int(r["Grid_Size_X"]) // wg, wg, int(r["LDS_Block_Size"]), int(r["VGPR_Count"]),
+               int(r["Scratch_Size"]))
+        groups.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    print(f"{'kernel':46s} {'grid':>6s} {'wg':>4s} {'LDS':>7s} {'VGPR':>5s} {'scr':>4s} {'calls':>6s} {'avg_us':>10s} {'min_us':>10s}")
+    for (short, grid, wg, lds, vgpr, scr), d in groups.items():
+        print(f"{short[:46]:46s} {grid:6d} {wg:4d} {lds:7d} {vgpr:5d} {scr:4d} {len(d):6d} {sum(d) / len(d):10.2f} {min(d):10.2f}")
+
+
 def inst_summary(path):
     """Instruction counts per gate+up launch: every FMA is one full-wave binary32 FMA per weight
     (N*K/64 wave instructions at M = 1) and no matrix-core instruction is issued."""
@@ -540,6 +619,9 @@ def main():
     if args.pmc_summary:
         pmc_summary(*args.pmc_summary)
         return
+    if args.group_trace:
+        group_trace(args.group_trace)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the library has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
@@ -567,6 +649,9 @@ def main():
         return
     if args.attention:
         run_attention_configs()
+        return
+    if args.floors:
+        run_floors()
         return
     stream = torch.cuda.current_stream()
 
@@ -694,13 +779,22 @@ def main():
             torch.cuda.synchronize()
             return a.elapsed_time(b) / R
 
+        def torch_scheme_step(i):
+            for L in layers:
+                wt = tmp[L["name"]]
+                rg.rg_cast_bf16_f32(L["ws"][i % len(L["ws"])], wt, stream=stream)
+                torch.matmul(L["xd"], wt.t(), out=L["y"])
+
         sms = timed(scheme_step)
+        tms = timed(torch_scheme_step)
         gms = timed(gemm_step)
-        scheme = dict(ms_per_step=round(sms, 4), gemm_only_ms_per_step=round(gms, 4),
-                      speedup_of_fused=round(sms / ms_per_step, 3),
+        best = min(sms, tms)
+        scheme = dict(ms_per_step=round(best, 4), capi_ms_per_step=round(sms, 4), torch_ms_per_step=round(tms, 4),
+                      gemm_only_ms_per_step=round(gms, 4), speedup_of_fused=round(best / ms_per_step, 3),
                       transient_fp32_bytes=int(max(4 * L["N"] * L["K"] for L in layers)),
-                      gemm="rg_linear_cast_baseline (exact cast, then rocBLAS sgemm); the GEMM-only figure is "
-                           "torch.matmul float32 on one resident FP32 copy")
+                      gemm="the faster of rg_linear_cast_baseline (exact cast, then rocBLAS sgemv at M=1) and "
+                           "the same cast followed by torch.matmul float32 (hipBLASLt); the GEMM-only figure is "
+                           "torch.matmul on one resident FP32 copy")
         del tmp
 
     # ---- CPU oracle on the host: bounded sample of the same step ----

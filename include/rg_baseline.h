@@ -5,7 +5,7 @@
  *
  * W is first widened into a transient FP32 copy (w_tmp_f32, 4NK bytes, owned
  * by the caller), then y = x * w_tmp^T by the vendor FP32 GEMM (rocBLAS sgemm,
- * a black box: its reduction order is the library's and may depend on the
+ * or sgemv for M = 1; a black box: its reduction order is the library's and may depend on the
  * device, the shape and the batch size, which is what the method removes).
  * It exists to time the scheme on the same buffers and stream as rg_linear;
  * it is never used by rg_linear.

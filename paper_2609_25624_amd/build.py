@@ -28,6 +28,10 @@ NEGCTL_SOURCES = ["rg_negctl.hip"]
 BASELINE_LIB = os.path.join(HERE, "librg_baseline.so")
 BASELINE_SOURCES = ["rg_baseline.cpp"]
 
+# The read-bandwidth probe the benchmark's floors are measured with (not the product path).
+PROBE_LIB = os.path.join(HERE, "librg_probe.so")
+PROBE_SOURCES = ["rg_probe.hip"]
+
 # A C program that uses the library through include/rg.h only (no Python).
 EXAMPLE_SRC = os.path.join(HERE, "examples", "linear_capi.c")
 EXAMPLE_BIN = os.path.join(HERE, "examples", "linear_capi")
@@ -36,6 +40,7 @@ EXAMPLE_BIN = os.path.join(HERE, "examples", "linear_capi")
 def build(verbose: bool = False) -> str:
     _build_lib(SOURCES, LIB, verbose)
     _build_lib(NEGCTL_SOURCES, NEGCTL_LIB, verbose)
+    _build_lib(PROBE_SOURCES, PROBE_LIB, verbose)
     rocm = os.path.dirname(os.path.dirname(os.path.realpath(HIPCC)))
     _build_lib(BASELINE_SOURCES, BASELINE_LIB, verbose,
                link=["-L" + HERE, "-lrg", "-L" + os.path.join(rocm, "lib"), "-lrocblas", "-Wl,-rpath,$ORIGIN",

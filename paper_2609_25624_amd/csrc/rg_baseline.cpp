@@ -50,9 +50,15 @@ extern "C" int rg_linear_cast_baseline(const float* x, const uint16_t* w, float*
     if (cs != RG_OK) return cs;
     if (rocblas_set_stream(hd.h, (hipStream_t)stream) != rocblas_status_success) return RG_ERR_HIP;
     const float one = 1.0f, zero = 0.0f;
-    // column-major view: y^T [N x M] = (w_tmp [N x K]) * (x^T [K x M]); w_tmp row-major is K x N column-major
-    const rocblas_status st = rocblas_sgemm(hd.h, rocblas_operation_transpose, rocblas_operation_none, (rocblas_int)N,
-                                            (rocblas_int)M, (rocblas_int)K, &one, wt, (rocblas_int)K, x,
-                                            (rocblas_int)K, &zero, y, (rocblas_int)N);
+    rocblas_status st;
+    if (M == 1) {
+        // one row of x: the vendor's matrix-vector product, y = (w_tmp viewed K x N column-major)^T x
+        st = rocblas_sgemv(hd.h, rocblas_operation_transpose, (rocblas_int)K, (rocblas_int)N, &one, wt, (rocblas_int)K,
+                           x, 1, &zero, y, 1);
+    } else {
+        // column-major view: y^T [N x M] = (w_tmp [N x K]) * (x^T [K x M]); w_tmp row-major is K x N column-major
+        st = rocblas_sgemm(hd.h, rocblas_operation_transpose, rocblas_operation_none, (rocblas_int)N, (rocblas_int)M,
+                           (rocblas_int)K, &one, wt, (rocblas_int)K, x, (rocblas_int)K, &zero, y, (rocblas_int)N);
+    }
     return st == rocblas_status_success ? RG_OK : RG_ERR_HIP;
 }

@@ -1631,22 +1631,37 @@ __device__ __forceinline__ bool better(float v, int64_t i, float bv, int64_t bi)
     return v > bv || (v == bv && i < bi);
 }
 
-__global__ void __launch_bounds__(256) argmax_kernel(const float* __restrict__ y, int64_t* __restrict__ out,
-                                                     int64_t N) {
-    __shared__ float sv[256];
-    __shared__ int64_t si[256];
+constexpr int kArgmaxThreads = 1024;
+constexpr int kArgmaxBatch = 16;     // independent loads in flight per thread
+
+__global__ void __launch_bounds__(kArgmaxThreads) argmax_kernel(const float* __restrict__ y, int64_t* __restrict__ out,
+                                                                int64_t N) {
+    __shared__ float sv[kArgmaxThreads];
+    __shared__ int64_t si[kArgmaxThreads];
     const int64_t m = blockIdx.x;
     const float* row = y + m * N;
     float bv = 0.0f;
     int64_t bi = -1;
-    for (int64_t n = threadIdx.x; n < N; n += 256) {
+    constexpr int64_t step = (int64_t)kArgmaxThreads * kArgmaxBatch;
+    int64_t n0 = threadIdx.x;
+    for (; n0 + (kArgmaxBatch - 1) * kArgmaxThreads < N; n0 += step) {
+        float v[kArgmaxBatch];
+#pragma unroll
+        for (int u = 0; u < kArgmaxBatch; ++u) v[u] = row[n0 + (int64_t)u * kArgmaxThreads];
+#pragma unroll
+        for (int u = 0; u < kArgmaxBatch; ++u) {
+            const int64_t n = n0 + (int64_t)u * kArgmaxThreads;
+            if (better(v[u], n, bv, bi)) { bv = v[u]; bi = n; }
+        }
+    }
+    for (int64_t n = n0; n < N; n += kArgmaxThreads) {
         const float v = row[n];
         if (better(v, n, bv, bi)) { bv = v; bi = n; }
     }
     sv[threadIdx.x] = bv;
     si[threadIdx.x] = bi;
     __syncthreads();
-    for (int h = 128; h > 0; h >>= 1) {
+    for (int h = kArgmaxThreads / 2; h > 0; h >>= 1) {
         if (threadIdx.x < h) {
             const float v = sv[threadIdx.x + h];
             const int64_t i = si[threadIdx.x + h];
@@ -1863,7 +1878,7 @@ hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t s
 }
 
 hipError_t launch_argmax(const float* y, int64_t* out, int64_t M, int64_t N, hipStream_t stream) {
-    hipLaunchKernelGGL(argmax_kernel, dim3((unsigned)M), dim3(256), 0, stream, y, out, N);
+    hipLaunchKernelGGL(argmax_kernel, dim3((unsigned)M), dim3(kArgmaxThreads), 0, stream, y, out, N);
     return hipGetLastError();
 }
 

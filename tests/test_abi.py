@@ -336,3 +336,15 @@ def test_inline_assembly_writes_no_register_asynchronously():
         blocks = re.findall(r";;#ASMSTART\n(.*?);;#ASMEND", asm, flags=re.S)
         ops = {ln.split()[0] for blk in blocks for ln in blk.splitlines() if ln.strip() and not ln.strip().startswith(";")}
         assert ops <= allowed, (f, sorted(ops - allowed))
+
+
+def test_probe_library_exports_and_host_checks():
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "rg_probe.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"^\s*int\s+(rg_\w+)\s*\(", text, flags=re.M)))
+    from paper_2609_25624_amd import probe
+    assert sorted(probe.EXPORTS) == names
+    L = probe.lib
+    assert L.rg_probe_read(None, 8192, 0x1000, 1, None) == 1
+    assert L.rg_probe_read(0x1000, 8000, 0x2000, 1, None) == 1          # not a multiple of 8 KB
+    assert L.rg_probe_read(0x1008, 8192, 0x2000, 1, None) == 1          # misaligned
+    assert L.rg_probe_read(0x1000, 8192, 0x2000, 0, None) == 1          # no workgroups
