@@ -78,8 +78,11 @@ typedef enum {
     RG_KERNEL_GEMV = 4,      /* M == 1, K % 256 == 0, K >= 4096: 32 KB W bursts, whole rows per wave */
     RG_KERNEL_STREAM = 5,    /* M <= 4: 8-row blocks of W streamed through LDS, one chain per lane
                                 (FP32 weights by default; BF16 weights when forced) */
-    RG_KERNEL_KTILE = 6      /* 4 < M <= 64 (any M when forced): 4 x 4 register tiles, K segments
+    RG_KERNEL_KTILE = 6,     /* 16 < M <= 64 (any M when forced): 4 x 4 register tiles, K segments
                                 shared out over thread groups */
+    RG_KERNEL_SKINNY = 7     /* 2 <= M <= 16: waves of 16 W rows x 4 segments, x of a segment
+                                shared by 16 lanes through DPP row broadcasts, slices of 2, 4 or
+                                8 rows of x */
 } rg_kernel_id;
 
 /* Scheduling overrides for the determinism tests.  0 in a field = planner
@@ -89,11 +92,13 @@ typedef enum {
  *                   (a kernel that cannot handle the shape is not forced; the
  *                    call returns RG_ERR_RANGE)
  *   waves_per_wg  : 1..8  waves (64 threads each) per workgroup (gemv: 1..4, and 1, 2
- *                   or 4 when K > 4096; ktile: 4, or 8 with tile_n 16)
+ *                   or 4 when K > 4096; ktile: 4, or 8 with tile_n 16; skinny: any count
+ *                   whose ceil(J / 4 / waves) segment groups per wave fit its registers)
  *   grid_wgs      : 1..65536 workgroups (work is spread over them evenly)
  *   depth         : 2..3  decode pipeline depth in 128-byte-per-row slabs (unused by gemv);
  *                   tiled kernel with 128 x 128 tiles: the build for 2 or 3 waves per SIMD;
- *                   ktile: 2 = 4 x 4, 3 = 4 x 8 outputs per thread (tile_n 32 or 64 only)
+ *                   ktile: 2 = 4 x 4, 3 = 4 x 8 outputs per thread (tile_n 32 or 64 only);
+ *                   skinny: 8 KB steps in flight per wave
  *   grid_order    : 0 = forward, 1 = reversed workgroup-to-rows mapping
  *   tile_n        : 0 = planner default, else 16, 32 or 64: ktile's W rows per tile
  *   reserved      : must be 0
@@ -118,8 +123,8 @@ typedef struct {
     int32_t grid_wgs;
     int32_t depth;         /* decode: pipeline depth; tiled 128 x 128: waves per SIMD (2 or 3);
                               ktile: 2 = 4 x 4, 3 = 4 x 8 outputs per thread */
-    int32_t rows_per_round;/* decode: W rows per workgroup round */
-    int32_t tile_m, tile_n;/* tiled: output tile */
+    int32_t rows_per_round;/* decode: W rows per workgroup round; skinny: 16 */
+    int32_t tile_m, tile_n;/* tiled: output tile; skinny: rows of x per slice, 16 W rows */
 } rg_plan_t;
 
 /*

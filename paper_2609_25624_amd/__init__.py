@@ -12,7 +12,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librg.so")
 
 RG_OK, RG_ERR_INVAL, RG_ERR_ALIGN, RG_ERR_ARCH, RG_ERR_HIP, RG_ERR_RANGE, RG_ERR_ALIAS = range(7)
-KERNELS = {0: "generic", 1: "decode", 2: "tiled", 3: "decode_xs", 4: "gemv", 5: "stream", 6: "ktile"}
+KERNELS = {0: "generic", 1: "decode", 2: "tiled", 3: "decode_xs", 4: "gemv", 5: "stream", 6: "ktile", 7: "skinny"}
 CHUNK = 256
 
 
@@ -183,7 +183,7 @@ def rg_linear_set_launch(cfg=None, **kw):
     c = rg_launch_t()
     for k, v in dict(cfg or {}, **kw).items():
         if k == "kernel" and isinstance(v, str):
-            v = {"generic": 1, "decode": 2, "tiled": 3, "decode_xs": 4, "gemv": 5, "stream": 6, "ktile": 7}[v]
+            v = {n: i + 1 for i, n in KERNELS.items()}[v]
         setattr(c, k, int(v))
     _check(lib.rg_linear_set_launch(ctypes.byref(c)), "rg_linear_set_launch")
 

@@ -69,6 +69,9 @@ struct Plan {
     int mslices = 1;
     int tile_m = 0, tile_n = 0;
     int cn = 4;          // ktile: W rows per thread's register tile (4 x cn outputs)
+    int spw = 0;         // skinny: segment groups per wave
+    int jp = 0;          // skinny: row stride of the LDS partials
+    int64_t groups = 0;  // skinny: row-group walkers per slice
 };
 
 // Largest decode pipeline depth whose LDS ring fits for a wave count.
@@ -227,6 +230,84 @@ bool ktile_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan*
     return true;
 }
 
+// Skinny kernel: slices of mt = 2, 4 or 8 rows of x, waves of 16 W rows x 4 segments with
+// x shared through DPP row broadcasts.  Each wave keeps x of spw segment groups in registers
+// (16 * mt * spw <= 128 floats), so nw = ceil(NSG / spw) <= 8 waves cover K.  Two waves per
+// SIMD: ceil(8 / nw) workgroups per CU where LDS allows.  Depth (steps in flight per wave):
+// the one that keeps the most bytes in flight per CU, 2 on a tie.
+constexpr int64_t kSkinnyMaxM = 16;
+constexpr int64_t kLdsBytes = 160 * 1024;
+
+bool skinny_shape_ok(int64_t M, int64_t K) {
+    return M >= 2 && K < ((int64_t)1 << 26);
+}
+
+bool skinny_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan* p) {
+    if (o.tile_n != 0) return false;
+    const int64_t J = ceil_div(K, rg::kChunk);
+    const int64_t NSG = ceil_div(J, 4);
+    int64_t spw, nw;
+    if (o.waves_per_wg > 0) {
+        nw = o.waves_per_wg;
+        spw = ceil_div(NSG, nw);
+    } else {
+        spw = ceil_div(NSG, 8);
+        if (spw == 3) spw = 4;
+        nw = ceil_div(NSG, spw);
+    }
+    if (spw == 3) spw = 4;
+    // the widest slice whose x registers fit (narrower slices read W once more each, mostly from L2)
+    int mt = M <= 2 ? 2 : (M <= 4 ? 4 : 8);
+    while (mt > 2 && mt * spw > 8) mt /= 2;
+    if (spw > 4 || mt * spw > 8) return false;
+    const int64_t S = ceil_div(M, mt);
+    if (S > 65536) return false;
+    const int64_t RG = ceil_div(N, 16);
+    int best_depth = 0;
+    int64_t best_g = 0;
+    double best_fly = -1.0;
+    int best_jp = 0;
+    for (int depth = 2; depth <= 3; ++depth) {
+        if (o.depth > 0 && depth != o.depth) continue;
+        // odd partial stride unless it costs a workgroup per CU
+        const int64_t lds_even = (int64_t)rg::skinny_lds_bytes(mt, (int)nw, depth, (int)J);
+        const int64_t lds_odd = (int64_t)rg::skinny_lds_bytes(mt, (int)nw, depth, (int)(J | 1));
+        const int jp = (lds_even > kLdsBytes || kLdsBytes / lds_odd == kLdsBytes / lds_even) ? (int)(J | 1) : (int)J;
+        const int64_t lds = jp == (int)J ? lds_even : lds_odd;
+        if (lds > kLdsBytes) continue;
+        int64_t wpc = kLdsBytes / lds;                  // workgroups per CU that LDS allows
+        const int64_t wave_cap = 8 / nw > 0 ? 8 / nw : 1;   // two waves per SIMD
+        if (wpc > wave_cap) wpc = wave_cap;
+        int64_t G = (o.grid_wgs > 0 ? o.grid_wgs : kNominalCUs * wpc) / S;   // walkers per slice
+        if (G < 1) G = 1;
+        if (G > RG) G = RG;
+        // bytes in flight per CU: resident workgroups x waves x depth
+        double res = (double)(G * S) / kNominalCUs;
+        if (res > (double)wpc) res = (double)wpc;
+        const double fly = res * (double)nw * depth;
+        if (fly > best_fly + 1e-9) {
+            best_fly = fly;
+            best_depth = depth;
+            best_g = G;
+            best_jp = jp;
+        }
+    }
+    if (best_depth == 0) return false;
+    p->mt = mt;
+    p->rq = 4;                 // reported as 16 W rows per row group
+    p->tile_m = mt;            // reported: rows of x per slice x W rows per group
+    p->tile_n = 16;
+    p->spw = (int)spw;
+    p->jp = best_jp;
+    p->nw = (int)nw;
+    p->depth = best_depth;
+    p->groups = best_g;
+    p->mslices = (int)S;
+    if (ceil_div(best_g, 8) * 8 * S > 0x7fffffff) return false;   // launched: padded to 8 per slice
+    p->grid = (int)(best_g * S);                                  // reported: workgroups with work
+    return true;
+}
+
 hipError_t launch_stream(const float* x, const void* w, const float* bias, float* y, int64_t M, int64_t N, int64_t K,
                          const Plan& p, bool f32_weights, hipStream_t st) {
     rg::StreamArgs a;
@@ -331,7 +412,9 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     // ktile from M = 9 on; for 5 <= M <= 8 only where its 16 x 16 tiles are many (measured:
     // the streaming decode kernel is faster on the narrow layers there)
     const bool ktile_pref = M > 8 || (M > 4 && ceil_div(N, 16) >= 384);
+    const bool skinny_ok = fast_ok && skinny_shape_ok(M, K);
     if (gemv_ok && ceil_div(K, rg::kChunk) == 16) want = RG_KERNEL_GEMV;
+    else if (skinny_ok && M <= kSkinnyMaxM) want = RG_KERNEL_SKINNY;
     else if (ktile_ok && ktile_pref) want = RG_KERNEL_KTILE;
     else if (decode_ok && M <= kDecodeMaxM) want = (M == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;
     else if (tiled_ok) want = RG_KERNEL_TILED;
@@ -344,10 +427,19 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         if (want == RG_KERNEL_GEMV && !gemv_ok) return RG_ERR_RANGE;
         if (want == RG_KERNEL_KTILE && !fast_ok) return RG_ERR_RANGE;   // any M when forced
         if (want == RG_KERNEL_STREAM && !(fast_ok && M <= 4)) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_SKINNY && !skinny_ok) return RG_ERR_RANGE;
     }
     p->mslices = 1;
     p->kernel = want;
     p->reverse = o.grid_order;
+    if (want == RG_KERNEL_SKINNY) {
+        if (skinny_schedule(M, N, K, o, p)) return RG_OK;
+        if (forced || o.waves_per_wg > 0 || o.grid_wgs > 0 || o.depth > 0) return RG_ERR_RANGE;
+        // x of a wave's segment groups does not fit its registers: the earlier kernels
+        p->mslices = 1;
+        want = p->kernel = (ktile_ok && ktile_pref) ? RG_KERNEL_KTILE
+                         : (decode_ok ? RG_KERNEL_DECODE : (tiled_ok ? RG_KERNEL_TILED : RG_KERNEL_GENERIC));
+    }
     if (want == RG_KERNEL_KTILE) {
         if (ktile_schedule(M, N, K, o, p)) return RG_OK;
         return RG_ERR_RANGE;
@@ -409,7 +501,7 @@ int make_plan_f32w(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launc
 }
 
 int validate_launch(const rg_launch_t& c) {
-    if (c.kernel < -1 || c.kernel > 7) return RG_ERR_RANGE;
+    if (c.kernel < -1 || c.kernel > 8) return RG_ERR_RANGE;
     if (c.tile_n != 0 && c.tile_n != 16 && c.tile_n != 32 && c.tile_n != 64) return RG_ERR_RANGE;
     if (c.reserved[0] != 0 || c.reserved[1] != 0) return RG_ERR_RANGE;
     if (c.waves_per_wg < 0 || c.waves_per_wg > 8) return RG_ERR_RANGE;
@@ -572,6 +664,23 @@ int linear_impl(const float* x, const uint16_t* w, const float* bias, float* y, 
         if (!p.x_streamed && blocks > 0x7fffffff) return RG_ERR_RANGE;
         e = p.x_streamed ? rg::launch_decode1(a, p.grid, p.nw, p.depth, st)
                          : rg::launch_decode(a, p.mt, (int)blocks, p.nw, p.depth, st);
+    } else if (p.kernel == RG_KERNEL_SKINNY) {
+        rg::SkinnyArgs a;
+        a.x = x;
+        a.w = w;
+        a.bias = bias;
+        a.y = y;
+        a.M = M;
+        a.N = N;
+        a.K = K;
+        a.RG = ceil_div(N, 16);
+        a.groups = p.groups;
+        a.J = (int)ceil_div(K, rg::kChunk);
+        a.NSG = (int)ceil_div(a.J, 4);
+        a.JP = p.jp;
+        a.mslices = p.mslices;
+        a.reverse = p.reverse;
+        e = rg::launch_skinny(a, p.mt, p.spw, p.nw, p.depth, st);
     } else if (p.kernel == RG_KERNEL_STREAM) {
         e = launch_stream(x, w, bias, y, M, N, K, p, false, st);
     } else if (p.kernel == RG_KERNEL_KTILE) {

@@ -52,6 +52,22 @@ struct StreamArgs {
     int reverse;          // reversed workgroup-to-block mapping
 };
 
+// Arguments of the skinny kernel (M >= 2, K % 8 == 0, K < 2^26, x and W 16-byte aligned).
+struct SkinnyArgs {
+    const float* x;
+    const uint16_t* w;
+    const float* bias;    // b[N] added after the fold, or null
+    float* y;
+    int64_t M, N, K;
+    int64_t RG;           // row groups of 16 W rows: ceil(N / 16)
+    int64_t groups;       // row-group walkers (workgroups) per slice
+    int J;                // segments: ceil(K / 256)
+    int NSG;              // segment groups of 4: ceil(J / 4)
+    int JP;               // row stride of the partials in LDS: J, or J | 1 (odd: no bank conflicts)
+    int mslices;          // slices of MT rows of x
+    int reverse;          // 1: walker g takes the row groups of walker groups-1-g, mirrored
+};
+
 hipError_t launch_generic(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N,
                           int64_t K, int grid, int reverse, hipStream_t stream);
 hipError_t launch_generic(const float* x, const float* w, const float* bias, float* y, int64_t M, int64_t N,
@@ -88,6 +104,12 @@ struct AttnArgs {
     uint32_t vmagic;                 // ceil(2^32 / (D / 8)) for D / 8 > 1 (row of a 16-byte vector)
 };
 hipError_t launch_attn(const AttnArgs& a, int cus, hipStream_t stream);
+
+// LDS bytes of a skinny launch (DEPTH steps of 8 KB per wave, then two sets of partials).
+inline size_t skinny_lds_bytes(int mt, int nw, int depth, int JP) {
+    return (size_t)nw * depth * 8192 + (size_t)2 * mt * 16 * JP * sizeof(float);
+}
+hipError_t launch_skinny(const SkinnyArgs& a, int mt, int spw, int nw, int depth, hipStream_t stream);
 
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream);
 hipError_t launch_argmax(const float* y, int64_t* out, int64_t M, int64_t N, hipStream_t stream);

@@ -1475,6 +1475,300 @@ __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// skinny kernel (2 <= M, K % 8 == 0): x shared by the 16 lanes of a DPP row.
+//
+// Work split.  W rows come in groups of 16 and K in groups of 4 segments.  A
+// wave works on one (row group, segment group) pair at a time: lane 16d + i
+// runs the chains of row 16 rg + i over segment 4 sg + d for the MT rows of x
+// that its workgroup's slice holds.  The 16 lanes of DPP row d share a segment,
+// so they share its x: lane i holds x[m][256 j + 16 i .. + 16) for each of the
+// MT rows, and the FMA that needs element 16 i + e reads it from lane i with a
+// row broadcast (row_newbcast) fused into v_fmac_f32.  x thus costs 16 MT
+// registers per segment group, a quarter of what a quad broadcast needs, and
+// the kernel runs two waves per SIMD.  Wave w of a workgroup of NW owns the
+// segment groups w, w + NW, ... (at most SPW of them, their x loaded once) and
+// the workgroup walks row groups g, g + G, ...; every segment group of a row
+// group is therefore computed inside one workgroup.
+//
+// Data path.  A step is 64 weights of each lane's chain: 16 rows x 4 segments
+// x 128 bytes = 8 KB, requested with 8 global->LDS DMA instructions (8 lanes
+// per 128-byte line) into a ring of DEPTH slots per wave.  The lane's 128-byte
+// image is XOR-swizzled by ((lane >> 1) & 7) in 16-byte units so that the
+// transposing ds_read_b128 are conflict-free; the step is read to registers,
+// the next-but-DEPTH step is requested into the freed slot, and the FMAs run
+// with DEPTH steps in flight.  All loads in flight in the stream are DMA loads
+// of the wave, which complete in issue order.
+//
+// Order.  A chain starts at +0 and runs its segment's weights in ascending k
+// (a short last segment stops at K).  Its partial goes to LDS; after the row
+// group's barrier one thread per (row of x, row of W) folds the J partials in
+// ascending segment order, adds b[n] for the bias variant and stores y.
+//
+// Slices.  With more than MT rows of x the grid holds ceil(M / MT) slices of
+// the workgroups; the slices of a row group sit 8 workgroups apart, are
+// dispatched to one XCD at about the same time and share its L2 for W.
+// ---------------------------------------------------------------------------
+constexpr int kSkSlabBytes = 8192;   // one step of a wave: 64 lanes x 128 bytes
+
+// acc[m] = fmaf(x_m[lane L of the row][E0 + h], w[h], acc[m]) for h = 0..3 (outer), m = 0..3
+template <int L, int E0>
+__device__ __forceinline__ void fmac_nb4(float (&acc)[4], const float (&X)[4][16], const float* w) {
+#define RG_G(A, X, W) "v_fmac_f32_dpp %" #A ", %" #X ", %" #W " row_newbcast:%24 row_mask:0xf bank_mask:0xf\n\t"
+    asm("s_nop 1\n\t"
+        RG_G(0, 4, 20) RG_G(1, 8, 20) RG_G(2, 12, 20) RG_G(3, 16, 20)
+        RG_G(0, 5, 21) RG_G(1, 9, 21) RG_G(2, 13, 21) RG_G(3, 17, 21)
+        RG_G(0, 6, 22) RG_G(1, 10, 22) RG_G(2, 14, 22) RG_G(3, 18, 22)
+        RG_G(0, 7, 23) RG_G(1, 11, 23) RG_G(2, 15, 23) RG_G(3, 19, 23)
+        : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3])
+        : "v"(X[0][E0]), "v"(X[0][E0 + 1]), "v"(X[0][E0 + 2]), "v"(X[0][E0 + 3]),
+          "v"(X[1][E0]), "v"(X[1][E0 + 1]), "v"(X[1][E0 + 2]), "v"(X[1][E0 + 3]),
+          "v"(X[2][E0]), "v"(X[2][E0 + 1]), "v"(X[2][E0 + 2]), "v"(X[2][E0 + 3]),
+          "v"(X[3][E0]), "v"(X[3][E0 + 1]), "v"(X[3][E0 + 2]), "v"(X[3][E0 + 3]),
+          "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "n"(L));
+#undef RG_G
+}
+
+// the same for two rows of x and h = 0..7
+template <int L, int E0>
+__device__ __forceinline__ void fmac_nb2(float (&acc)[2], const float (&X)[2][16], const float* w) {
+#define RG_G(A, X, W) "v_fmac_f32_dpp %" #A ", %" #X ", %" #W " row_newbcast:%26 row_mask:0xf bank_mask:0xf\n\t"
+    asm("s_nop 1\n\t"
+        RG_G(0, 2, 18) RG_G(1, 10, 18) RG_G(0, 3, 19) RG_G(1, 11, 19)
+        RG_G(0, 4, 20) RG_G(1, 12, 20) RG_G(0, 5, 21) RG_G(1, 13, 21)
+        RG_G(0, 6, 22) RG_G(1, 14, 22) RG_G(0, 7, 23) RG_G(1, 15, 23)
+        RG_G(0, 8, 24) RG_G(1, 16, 24) RG_G(0, 9, 25) RG_G(1, 17, 25)
+        : "+v"(acc[0]), "+v"(acc[1])
+        : "v"(X[0][E0]), "v"(X[0][E0 + 1]), "v"(X[0][E0 + 2]), "v"(X[0][E0 + 3]),
+          "v"(X[0][E0 + 4]), "v"(X[0][E0 + 5]), "v"(X[0][E0 + 6]), "v"(X[0][E0 + 7]),
+          "v"(X[1][E0]), "v"(X[1][E0 + 1]), "v"(X[1][E0 + 2]), "v"(X[1][E0 + 3]),
+          "v"(X[1][E0 + 4]), "v"(X[1][E0 + 5]), "v"(X[1][E0 + 6]), "v"(X[1][E0 + 7]),
+          "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "v"(w[4]), "v"(w[5]), "v"(w[6]), "v"(w[7]), "n"(L));
+#undef RG_G
+}
+
+// the same for eight rows of x and h = 0..1
+template <int L, int E0>
+__device__ __forceinline__ void fmac_nb8(float (&acc)[8], const float (&X)[8][16], const float* w) {
+#define RG_G(A, X, W) "v_fmac_f32_dpp %" #A ", %" #X ", %" #W " row_newbcast:%26 row_mask:0xf bank_mask:0xf\n\t"
+    asm("s_nop 1\n\t"
+        RG_G(0, 8, 24) RG_G(1, 10, 24) RG_G(2, 12, 24) RG_G(3, 14, 24)
+        RG_G(4, 16, 24) RG_G(5, 18, 24) RG_G(6, 20, 24) RG_G(7, 22, 24)
+        RG_G(0, 9, 25) RG_G(1, 11, 25) RG_G(2, 13, 25) RG_G(3, 15, 25)
+        RG_G(4, 17, 25) RG_G(5, 19, 25) RG_G(6, 21, 25) RG_G(7, 23, 25)
+        : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(acc[4]), "+v"(acc[5]), "+v"(acc[6]),
+          "+v"(acc[7])
+        : "v"(X[0][E0]), "v"(X[0][E0 + 1]), "v"(X[1][E0]), "v"(X[1][E0 + 1]),
+          "v"(X[2][E0]), "v"(X[2][E0 + 1]), "v"(X[3][E0]), "v"(X[3][E0 + 1]),
+          "v"(X[4][E0]), "v"(X[4][E0 + 1]), "v"(X[5][E0]), "v"(X[5][E0 + 1]),
+          "v"(X[6][E0]), "v"(X[6][E0 + 1]), "v"(X[7][E0]), "v"(X[7][E0 + 1]),
+          "v"(w[0]), "v"(w[1]), "n"(L));
+#undef RG_G
+}
+
+// The FMAs of piece t (weights 8t .. 8t+7 of the lane's 64) of step s of a segment: segment
+// element 64 s + 8 t + h, whose x sits in lane 4 s + t / 2 of the row, register 8 (t & 1) + h.
+template <int MT, int S, int T>
+__device__ __forceinline__ void sk_piece(float (&acc)[MT], const float (&X)[MT][16], const uint4& p) {
+    const uint32_t d[4] = {p.x, p.y, p.z, p.w};
+    float wv[8];
+#pragma unroll
+    for (int h = 0; h < 8; ++h) wv[h] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
+    constexpr int L = 4 * S + T / 2, E0 = 8 * (T & 1);
+    if constexpr (MT == 2) {
+        fmac_nb2<L, E0>(acc, X, wv);
+    } else if constexpr (MT == 4) {
+        fmac_nb4<L, E0>(acc, X, wv);
+        fmac_nb4<L, E0 + 4>(acc, X, &wv[4]);
+    } else {
+        fmac_nb8<L, E0>(acc, X, wv);
+        fmac_nb8<L, E0 + 2>(acc, X, &wv[2]);
+        fmac_nb8<L, E0 + 4>(acc, X, &wv[4]);
+        fmac_nb8<L, E0 + 6>(acc, X, &wv[6]);
+    }
+}
+
+// One step: the 8 pieces in order; GUARD: only the first np pieces (a short last segment,
+// np the same on the 16 lanes of a row, or 0 on a row past the last segment).
+template <int MT, int S, bool GUARD>
+__device__ __forceinline__ void sk_step(float (&acc)[MT], const float (&X)[MT][16], const uint4 (&wp)[8], int np) {
+    if (!GUARD || np > 0) sk_piece<MT, S, 0>(acc, X, wp[0]);
+    if (!GUARD || np > 1) sk_piece<MT, S, 1>(acc, X, wp[1]);
+    if (!GUARD || np > 2) sk_piece<MT, S, 2>(acc, X, wp[2]);
+    if (!GUARD || np > 3) sk_piece<MT, S, 3>(acc, X, wp[3]);
+    if (!GUARD || np > 4) sk_piece<MT, S, 4>(acc, X, wp[4]);
+    if (!GUARD || np > 5) sk_piece<MT, S, 5>(acc, X, wp[5]);
+    if (!GUARD || np > 6) sk_piece<MT, S, 6>(acc, X, wp[6]);
+    if (!GUARD || np > 7) sk_piece<MT, S, 7>(acc, X, wp[7]);
+}
+
+template <int MT, int SPW, int DEPTH>
+__global__ void __launch_bounds__(512) skinny_kernel(SkinnyArgs a) {
+    static_assert(MT == 2 || MT == 4 || MT == 8, "rows of x per slice");
+    static_assert(SPW >= 1 && MT * SPW <= 8, "x registers: 16 * MT * SPW <= 128");
+    static_assert(DEPTH >= 2 && DEPTH <= 3, "ring depth");
+    extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int NW = (int)(blockDim.x >> 6);
+    const int d = lane >> 4, i = lane & 15;
+    const int J = a.J, NSG = a.NSG;
+    const int64_t N = a.N, K = a.K, RG = a.RG;
+    const int64_t row_bytes = 2 * K;
+
+    // workgroup -> (slice, row-group walker g); slices of one g sit 8 workgroups apart
+    int64_t g;
+    int slice;
+    {
+        const int64_t b = blockIdx.x;
+        const int S = a.mslices;
+        slice = (int)((b >> 3) % S);
+        g = ((b >> 3) / S) * 8 + (b & 7);
+        if (g >= a.groups) return;                        // padding workgroup: no work
+    }
+    const int64_t G = a.groups;
+    const float* xs = a.x + (int64_t)slice * MT * K;
+    float* ys = a.y + (int64_t)slice * MT * N;
+    const int64_t Ms = a.M - (int64_t)slice * MT;         // rows of x in this slice (>= 1)
+    const int nrg = (int)((RG - g + G - 1) / G);          // row groups of this workgroup
+    const int nsg = wave < NSG ? min(SPW, (NSG - 1 - wave) / NW + 1) : 0;   // this wave's segment groups
+    const int tpr = 4 * nsg;                              // steps per row group
+    const int nsteps = nrg * tpr;
+
+    uint8_t* ring = sk_lds + (size_t)wave * DEPTH * kSkSlabBytes;
+    // partials [2][MT][16][JP]: an odd row stride JP puts the 16 rows of a write in distinct banks
+    float* part = reinterpret_cast<float*>(sk_lds + (size_t)NW * DEPTH * kSkSlabBytes);
+    const int JP = a.JP;
+    const uint32_t ring_base = lds_addr(ring);
+    const int last_len = (int)(K - (int64_t)(J - 1) * kChunk);   // weights of the last segment
+
+    // DMA roles: instruction t fills consumer lanes 8t .. 8t+7 (row 8 (t & 1) + (lane >> 3) of
+    // the group, segment 4 sg + t / 2); this lane brings piece u of that consumer's 64 weights
+    const int ic0 = lane >> 3, ic1 = 8 + (lane >> 3);
+    const int u0 = (lane & 7) ^ (lane >> 4), u1 = (lane & 7) ^ (4 + (lane >> 4));
+
+    auto row_group = [&](int r) -> int64_t {
+        const int64_t rgi = g + (int64_t)r * G;
+        return a.reverse ? RG - 1 - rgi : rgi;
+    };
+    auto issue = [&](int st) {
+        const int r = st / tpr;
+        const int qs = st - r * tpr;
+        const int sg = wave + NW * (qs >> 2), s = qs & 3;
+        const int64_t n0 = 16 * row_group(r);
+        const char* base = reinterpret_cast<const char*>(a.w) + n0 * row_bytes;
+        const int rmax = (int)min((int64_t)15, N - 1 - n0);
+        const uint32_t slot = ring_base + (uint32_t)((st % DEPTH) * kSkSlabBytes);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int row = min((t & 1) ? ic1 : ic0, rmax);
+            const int j = min(4 * sg + (t >> 1), J - 1);
+            const int jlen = (j == J - 1) ? last_len : kChunk;
+            int e = 64 * s + 8 * ((t & 1) ? u1 : u0);
+            if (e >= jlen) e = 0;                         // past a short last segment: never read
+            const uint32_t voff = (uint32_t)(row * row_bytes) + (uint32_t)(j * (2 * kChunk) + 2 * e);
+            dma16(base, voff, slot + 1024u * t);
+        }
+    };
+
+    // prologue: the first DEPTH steps in flight, then x of this wave's segment groups
+#pragma unroll
+    for (int st = 0; st < DEPTH; ++st)
+        if (st < nsteps) issue(st);
+    float X[SPW][MT][16];
+#pragma unroll
+    for (int q = 0; q < SPW; ++q) {
+        const int j = 4 * (wave + NW * q) + d;
+        const int64_t kb = (int64_t)j * kChunk + 16 * i;
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                // unconditional load from a clamped address, then zero what is outside x
+                const bool ok = q < nsg && j < J && m < Ms && kb + 4 * c + 4 <= K;
+                const float4 v = *reinterpret_cast<const float4*>(xs + (ok ? (int64_t)m * K + kb + 4 * c : 0));
+                X[q][m][4 * c + 0] = ok ? v.x : 0.0f;
+                X[q][m][4 * c + 1] = ok ? v.y : 0.0f;
+                X[q][m][4 * c + 2] = ok ? v.z : 0.0f;
+                X[q][m][4 * c + 3] = ok ? v.w : 0.0f;
+            }
+    }
+    // Everything issued so far has landed: from here on the only loads this wave has in
+    // flight in the stream are its DMA steps (the fold's bias loads are waited for at once).
+    vmcnt_wait<0>();
+
+    const uint8_t* rd = ring + 128 * lane;
+    const int sw = (lane >> 1) & 7;
+    int st = 0;
+    for (int r = 0; r < nrg; ++r) {
+        const int64_t n0 = 16 * row_group(r);
+        const int par = r & 1;
+        for (int q = 0; q < nsg; ++q) {
+            const int sg = wave + NW * q;
+            const int j = 4 * sg + d;
+            const int len = j < J ? (j == J - 1 ? last_len : kChunk) : 0;
+            // every row of the wave has 4 whole segments here: no guards
+            const bool whole = 4 * sg + 4 < J || (4 * sg + 4 == J && last_len == kChunk);
+            float acc[MT];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) acc[m] = 0.0f;
+            auto step = [&](auto sc) {
+                constexpr int s = decltype(sc)::value;
+                const int ahead = min(DEPTH - 1, nsteps - 1 - st);
+                if (ahead >= 2) vmcnt_wait<16>();
+                else if (ahead == 1) vmcnt_wait<8>();
+                else vmcnt_wait<0>();
+                const uint8_t* src = rd + (st % DEPTH) * kSkSlabBytes;
+                uint4 wp[8];
+#pragma unroll
+                for (int t = 0; t < 8; ++t) wp[t] = *reinterpret_cast<const uint4*>(src + 16 * (t ^ sw));
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                if (st + DEPTH < nsteps) issue(st + DEPTH);
+                const int np = min(8, max(0, (len - 64 * s) / 8));
+#define RG_SK_STEP(Q)                                                          \
+    if (whole) sk_step<MT, s, false>(acc, X[Q], wp, 8);                        \
+    else sk_step<MT, s, true>(acc, X[Q], wp, np);
+                if constexpr (SPW == 1) {
+                    RG_SK_STEP(0)
+                } else if constexpr (SPW == 2) {
+                    if (q == 0) { RG_SK_STEP(0) } else { RG_SK_STEP(1) }
+                } else {
+                    switch (q) {
+                        case 0: RG_SK_STEP(0) break;
+                        case 1: RG_SK_STEP(1) break;
+                        case 2: RG_SK_STEP(2) break;
+                        default: RG_SK_STEP(3) break;
+                    }
+                }
+#undef RG_SK_STEP
+                ++st;
+            };
+            step(std::integral_constant<int, 0>{});
+            step(std::integral_constant<int, 1>{});
+            step(std::integral_constant<int, 2>{});
+            step(std::integral_constant<int, 3>{});
+            if (j < J) {
+#pragma unroll
+                for (int m = 0; m < MT; ++m) part[((par * MT + m) * 16 + i) * JP + j] = acc[m];
+            }
+        }
+        __syncthreads();
+        // fold: one thread per (row of x, row of W); part[par] is written again only after the
+        // next row group's barrier, which every thread reaches after this fold
+        for (int o = tid; o < 16 * MT; o += 64 * NW) {
+            const int m = o >> 4, ii = o & 15;
+            const int64_t n = n0 + ii;
+            if (m < Ms && n < N) {
+                float v = fold_partials(&part[((par * MT + m) * 16 + ii) * JP], J);
+                if (a.bias) v = v + a.bias[n];
+                ys[(int64_t)m * N + n] = v;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // stream kernel (M <= MT <= 4; FP32 or BF16 weights): streaming GEMV / skinny GEMM.
 //
 // Work split.  Rows of W come in blocks of 8; workgroup b takes blocks b, b + G,
@@ -1867,6 +2161,44 @@ static hipError_t launch_stream_t(const StreamArgs& a, int mt, int grid, hipStre
 
 hipError_t launch_stream(const StreamArgs& a, bool f32_weights, int mt, int grid, hipStream_t stream) {
     return f32_weights ? launch_stream_t<float>(a, mt, grid, stream) : launch_stream_t<uint16_t>(a, mt, grid, stream);
+}
+
+template <int MT, int SPW, int DEPTH>
+static hipError_t launch_skinny_t(const SkinnyArgs& a, int nw, hipStream_t stream) {
+    const size_t dyn = skinny_lds_bytes(MT, nw, DEPTH, a.JP);
+    static bool attr = false;   // raise the dynamic-LDS limit once per build of the kernel
+    if (!attr) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<MT, SPW, DEPTH>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e != hipSuccess) return e;
+        attr = true;
+    }
+    const int64_t blocks = (a.groups + 7) / 8 * 8 * a.mslices;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((skinny_kernel<MT, SPW, DEPTH>), dim3((unsigned)blocks), dim3(nw * 64), dyn, stream, a);
+    return hipGetLastError();
+}
+
+template <int MT, int SPW>
+static hipError_t launch_skinny_d(const SkinnyArgs& a, int nw, int depth, hipStream_t stream) {
+    if (depth == 2) return launch_skinny_t<MT, SPW, 2>(a, nw, stream);
+    if (depth == 3) return launch_skinny_t<MT, SPW, 3>(a, nw, stream);
+    return hipErrorInvalidValue;
+}
+
+// Rows of x per slice (2, 4 or 8) and segment groups per wave (x registers: 16 * mt * spw <= 128).
+hipError_t launch_skinny(const SkinnyArgs& a, int mt, int spw, int nw, int depth, hipStream_t stream) {
+    if (nw < 1 || nw > 8 || a.JP < a.J || skinny_lds_bytes(mt, nw, depth, a.JP) > 160 * 1024) return hipErrorInvalidValue;
+    if ((int64_t)nw * spw < a.NSG) return hipErrorInvalidValue;   // every segment group has a wave
+    switch (mt * 10 + spw) {
+        case 21: return launch_skinny_d<2, 1>(a, nw, depth, stream);
+        case 22: return launch_skinny_d<2, 2>(a, nw, depth, stream);
+        case 24: return launch_skinny_d<2, 4>(a, nw, depth, stream);
+        case 41: return launch_skinny_d<4, 1>(a, nw, depth, stream);
+        case 42: return launch_skinny_d<4, 2>(a, nw, depth, stream);
+        case 81: return launch_skinny_d<8, 1>(a, nw, depth, stream);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_cast(const uint16_t* w, float* o, int64_t count, hipStream_t stream) {

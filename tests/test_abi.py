@@ -126,7 +126,7 @@ def test_tiled_128_build_choice():
 
 
 def test_set_launch_range_checks():
-    for bad in (dict(waves_per_wg=9), dict(grid_wgs=-1), dict(depth=4), dict(depth=1), dict(grid_order=2), dict(kernel=8), dict(tile_n=48)):
+    for bad in (dict(waves_per_wg=9), dict(grid_wgs=-1), dict(depth=4), dict(depth=1), dict(grid_order=2), dict(kernel=9), dict(tile_n=48)):
         with pytest.raises(rg.RgError) as e:
             rg.rg_linear_set_launch(**bad)
         assert e.value.code == rg.RG_ERR_RANGE

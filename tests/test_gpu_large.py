@@ -16,13 +16,23 @@ pytestmark = pytest.mark.gpu
 _R = 1021
 
 
-@pytest.mark.parametrize("M,N,K,kernel", [(1, 1048579, 2304, "decode_xs"), (1, 524309, 4096, "gemv"),
-                                          (3, 1048579, 2304, "decode"), (16, 1048579, 2304, "ktile"),
-                                          (70, 1048579, 2304, "tiled")])
-def test_weights_beyond_4_gib(M, N, K, kernel):
+@pytest.fixture(autouse=True)
+def _reset_launch():
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(None)
+    yield
+    rg.rg_linear_set_launch(None)
+
+
+@pytest.mark.parametrize("M,N,K,kernel,forced", [(1, 1048579, 2304, "decode_xs", False), (1, 524309, 4096, "gemv", False),
+                                                 (3, 1048579, 2304, "skinny", False), (16, 1048579, 2304, "skinny", False),
+                                                 (3, 1048579, 2304, "decode", True), (16, 1048579, 2304, "ktile", True),
+                                                 (70, 1048579, 2304, "tiled", False)])
+def test_weights_beyond_4_gib(M, N, K, kernel, forced):
     import torch
     import paper_2609_25624_amd as rg
     assert 2 * N * K > (1 << 32)
+    rg.rg_linear_set_launch(kernel=kernel) if forced else rg.rg_linear_set_launch(None)
     plan = rg.rg_plan(M, N, K)
     assert plan["kernel_name"] == kernel
     gu.log(f"large W: M={M} N={N} K={K} ({2 * N * K / 2**30:.2f} GiB) kernel={kernel}")

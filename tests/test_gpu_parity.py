@@ -420,6 +420,10 @@ def _launch_settings():
         dict(kernel="ktile", tile_n=64, depth=3, grid_order=1),
         dict(kernel="stream"),
         dict(kernel="stream", grid_wgs=7, grid_order=1),
+        dict(kernel="skinny"),
+        dict(kernel="skinny", depth=3, grid_order=1),
+        dict(kernel="skinny", depth=2, grid_wgs=5),
+        dict(kernel="skinny", waves_per_wg=8, grid_wgs=1000, grid_order=1),
     ]
 
 

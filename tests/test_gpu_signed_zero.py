@@ -91,6 +91,7 @@ def _kernel_cases():
         ("ktile", 5, 130, 1000), ("ktile", 16, 301, 4104), ("ktile", 64, 77, 520),
         ("stream", 1, 33, 264), ("stream", 4, 130, 4352),
         ("tiled", 100, 1000, 1000), ("tiled", 129, 257, 264),
+        ("skinny", 2, 33, 264), ("skinny", 4, 1030, 4104), ("skinny", 9, 77, 1000), ("skinny", 16, 130, 4096),
     ]
 
 
