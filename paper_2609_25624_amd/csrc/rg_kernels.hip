@@ -122,17 +122,61 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // Issued through inline asm so the compiler does not add its conservative
 // vmcnt(0) before every LDS read; the kernel waits with vmcnt_wait<N>().
 // M0 (which holds the LDS address for the DMA and is read when the
-// instruction issues) is saved and restored around it.
+// instruction issues) is saved and restored around it.  On this generation an
+// LDS DMA must not read M0 in the cycle after a scalar write of M0 (one wait
+// state, which the compiler inserts for its own DMA but cannot see inside
+// inline asm): the s_nop provides it.
 __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
     uint32_t saved;
     asm volatile(
         "s_mov_b32 %0, m0\n\t"
         "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
         "global_load_lds_dwordx4 %1, %3\n\t"
         "s_mov_b32 m0, %0\n\t"
         : "=&s"(saved)
         : "v"(voff), "s"(lds_base), "s"(sbase)
         : "memory");
+}
+
+// Eight DMA instructions into LDS [lds_base + 1024 t, + 1024), t = 0..7, from
+// sbase + vo[t]: the skinny kernel's step with no clamping (whole row group, whole
+// segments), with no vector instruction spent on addresses (vo[] is loop-invariant).
+// Same M0 handling as dma16.  (The instruction's immediate offset is not used: it
+// would move the LDS destination as well.)
+__device__ __forceinline__ void dma8(const void* sbase, const uint32_t (&vo)[8], uint32_t lds_base) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %9\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %10\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, %10\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %3, %10\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %4, %10\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %5, %10\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %6, %10\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %7, %10\n\t"
+        "s_add_u32 m0, m0, 0x400\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %8, %10\n\t"
+        "s_mov_b32 m0, %0\n\t"
+        : "=&s"(saved)
+        : "v"(vo[0]), "v"(vo[1]), "v"(vo[2]), "v"(vo[3]), "v"(vo[4]), "v"(vo[5]), "v"(vo[6]), "v"(vo[7]),
+          "s"(lds_base), "s"(sbase)
+        : "memory", "scc");
 }
 
 // Wait until at most N vector-memory operations of this wave are outstanding.
@@ -1652,6 +1696,12 @@ __global__ void __launch_bounds__(512) skinny_kernel(SkinnyArgs a) {
         const int64_t rgi = g + (int64_t)r * G;
         return a.reverse ? RG - 1 - rgi : rgi;
     };
+    // unclamped DMA offsets of this lane past a step's base: instruction t reads row ic,
+    // segment t / 2 of the group, piece u
+    uint32_t vo[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+        vo[t] = (uint32_t)(((t & 1) ? ic1 : ic0) * row_bytes) + 512u * (t >> 1) + 16u * ((t & 1) ? u1 : u0);
     auto issue = [&](int st) {
         const int r = st / tpr;
         const int qs = st - r * tpr;
@@ -1660,6 +1710,10 @@ __global__ void __launch_bounds__(512) skinny_kernel(SkinnyArgs a) {
         const char* base = reinterpret_cast<const char*>(a.w) + n0 * row_bytes;
         const int rmax = (int)min((int64_t)15, N - 1 - n0);
         const uint32_t slot = ring_base + (uint32_t)((st % DEPTH) * kSkSlabBytes);
+        if (rmax == 15 && (4 * sg + 4 < J || (4 * sg + 4 == J && last_len == kChunk))) {
+            dma8(base + (int64_t)(4 * sg * kChunk + 64 * s) * 2, vo, slot);
+            return;
+        }
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
             const int row = min((t & 1) ? ic1 : ic0, rmax);

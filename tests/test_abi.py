@@ -330,12 +330,28 @@ def test_inline_assembly_writes_no_register_asynchronously():
     before then (a build that loaded x this way reused a pending destination for a load address,
     and faulted).  The only memory instruction the library's inline assembly may issue is the
     global->LDS DMA (no register destination); every other asm instruction is synchronous."""
-    allowed = {"s_nop", "s_mov_b32", "global_load_lds_dwordx4", "s_waitcnt", "v_fmac_f32_dpp"}
+    allowed = {"s_nop", "s_mov_b32", "s_add_u32", "global_load_lds_dwordx4", "s_waitcnt", "v_fmac_f32_dpp"}
     for f in ("rg_kernels.hip", "rg_attn.hip"):
         asm = _device_asm(f)
         blocks = re.findall(r";;#ASMSTART\n(.*?);;#ASMEND", asm, flags=re.S)
         ops = {ln.split()[0] for blk in blocks for ln in blk.splitlines() if ln.strip() and not ln.strip().startswith(";")}
         assert ops <= allowed, (f, sorted(ops - allowed))
+
+
+def test_inline_lds_dma_never_reads_m0_right_after_writing_it():
+    """On this generation an LDS DMA needs one wait state after a scalar write of M0 (its LDS
+    address); the compiler inserts it for DMA it emits itself, not inside inline assembly.
+    Every global_load_lds in the library's inline assembly follows an instruction that is not
+    an M0 write."""
+    n = 0
+    for f in ("rg_kernels.hip", "rg_attn.hip"):
+        for blk in re.findall(r";;#ASMSTART\n(.*?);;#ASMEND", _device_asm(f), flags=re.S):
+            lines = [ln.strip() for ln in blk.splitlines() if ln.strip() and not ln.strip().startswith(";")]
+            for i, ln in enumerate(lines):
+                if ln.startswith("global_load_lds"):
+                    n += 1
+                    assert i > 0 and not re.match(r"s_\w+\s+m0,", lines[i - 1]), (f, lines[max(0, i - 2):i + 1])
+    assert n > 0
 
 
 def test_probe_library_exports_and_host_checks():
