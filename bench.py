@@ -70,6 +70,10 @@ def parse():
     ap.add_argument("--floors", action="store_true",
                     help="read floors of the M=1 Llama-3-8B layers: librg_probe's read kernel over exactly the "
                          "layer's weight bytes, cold (the same rotation as the benchmark), one JSON line each")
+    ap.add_argument("--fma-rates", action="store_true",
+                    help="binary32 FMA issue rates of librg_probe's FMA kernel: plain, DPP row broadcast and DPP "
+                         "quad broadcast first operand, 8 and 16 chains per thread, 1 to 3 waves per SIMD; one JSON "
+                         "line each")
     ap.add_argument("--profile-kernels", action="store_true",
                     help="short run for hardware counters: 20 launches of the gate+up M=1 layer, then 5 plain "
                          "device copies of 256 MiB (the calibration kernel for HBM byte counters)")
@@ -103,6 +107,41 @@ def profile_kernels():
     torch.cuda.synchronize()
     print(json.dumps({"profiled": "gate_up decode x20, copy 256MiB x5", "copy_bytes": 256 << 20,
                       "decode_algorithmic_bytes": 2 * N * K + 4 * K + 4 * N}), flush=True)
+
+
+def run_fma_rates():
+    """TFLOP/s of librg_probe's FMA kernel (independent v_fmac_f32 chains, the forms the linear-layer
+    kernels issue) at 1, 2 and 3 waves per SIMD (256, 512, 768 workgroups of 4 waves on 256 CUs).
+    Best of 3 loops of 5 launches."""
+    import torch
+
+    from paper_2609_25624_amd import probe
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    out = torch.empty(768 * 256, dtype=torch.float32, device=dev)
+    iters = 4096
+    for mode, mname in ((0, "plain"), (1, "dpp_row_newbcast"), (2, "dpp_quad_perm")):
+        for chains in (8, 16):
+            for grid in (256, 512, 768):
+                probe.rg_probe_fma(mode, chains, out, grid, iters, stream=stream)
+                torch.cuda.synchronize()
+                best = None
+                for rep in range(3):
+                    a = torch.cuda.Event(enable_timing=True)
+                    b = torch.cuda.Event(enable_timing=True)
+                    a.record(stream)
+                    for _ in range(5):
+                        probe.rg_probe_fma(mode, chains, out, grid, iters, stream=stream)
+                    b.record(stream)
+                    torch.cuda.synchronize()
+                    ms = a.elapsed_time(b) / 5
+                    best = ms if best is None else min(best, ms)
+                flops = 2.0 * 64 * iters * grid * 256
+                tf = flops / (best * 1e-3) / 1e12
+                print(json.dumps({"fma": mname, "chains_per_thread": chains, "waves_per_simd": grid // 256,
+                                  "TFLOPs": round(tf, 2), "frac_of_fp32_157": round(tf / 157.3, 3),
+                                  "fma_instr_per_cycle_per_simd_at_2.4GHz": round(tf * 1e12 / 2 / 64 / 1024 / 2.4e9, 3)}),
+                      flush=True)
 
 
 def run_floors():
@@ -652,6 +691,9 @@ def main():
         return
     if args.floors:
         run_floors()
+        return
+    if args.fma_rates:
+        run_fma_rates()
         return
     stream = torch.cuda.current_stream()
 

@@ -14,6 +14,15 @@
  *          with the XOR of the words the thread read (keeps the loads alive)
  *   grid   workgroups of 256 threads, 1 .. 65536
  * Returns 0, 1 on an invalid argument, 4 on a launch error.
+ *
+ * rg_probe_fma: the binary32 FMA issue rate the kernels can reach, for the
+ * ceilings they are held against.  Every thread of grid workgroups of 256 runs
+ * `chains` (8 or 16) independent v_fmac_f32 chains for iters * 64 steps, each
+ * FMA's first operand read plainly (mode 0), through a DPP row broadcast
+ * (mode 1) or a DPP quad broadcast (mode 2), the forms the kernels use; 2 * 64 *
+ * iters * grid * 256 flops per launch.  out: device pointer to grid * 256
+ * floats (the chains' sums).  Returns 0, 1 on an invalid argument, 4 on a
+ * launch error.
  */
 #ifndef RG_PROBE_H
 #define RG_PROBE_H
@@ -25,6 +34,7 @@ extern "C" {
 #endif
 
 int rg_probe_read(const void* src, int64_t bytes, uint32_t* sink, int32_t grid, void* stream);
+int rg_probe_fma(int32_t mode, int32_t chains, float* out, int32_t grid, int32_t iters, void* stream);
 
 #ifdef __cplusplus
 }

@@ -38,7 +38,59 @@ __global__ void __launch_bounds__(256) read_kernel(const uint4* __restrict__ src
     sink[(int64_t)blockIdx.x * 256 + threadIdx.x] = acc;
 }
 
+// FMA issue-rate probe: CH independent accumulator chains per thread, each step one
+// v_fmac_f32 per chain with its first operand read plainly (MODE 0), through a DPP row
+// broadcast (MODE 1, row_newbcast) or a DPP quad broadcast (MODE 2, quad_perm), as the
+// linear-layer kernels use them.  The operands are non-trivial values near 1 (so the
+// arithmetic switches as much as real data does).
+template <int CH, int MODE>
+__global__ void __launch_bounds__(256) fma_kernel(float* out, int iters) {
+    float a[CH];
+#pragma unroll
+    for (int i = 0; i < CH; ++i) a[i] = threadIdx.x * 1e-3f + i;
+    const float xs[4] = {1.0001f + threadIdx.x * 1e-9f, 0.9999f, 1.00002f, 0.99998f};
+    const float w0 = 0.5f + threadIdx.x * 1e-7f, w1 = 0.25f;
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int r = 0; r < 64 / CH; ++r) {
+            if (MODE != 0) asm volatile("s_nop 1");   // the wait states a DPP read of a fresh VGPR needs
+#pragma unroll
+            for (int i = 0; i < CH; ++i) {
+                if constexpr (MODE == 0)
+                    asm volatile("v_fmac_f32 %0, %1, %2" : "+v"(a[i]) : "v"(xs[i & 3]), "v"((i & 4) ? w0 : w1));
+                else if constexpr (MODE == 1)
+                    asm volatile("v_fmac_f32_dpp %0, %1, %2 row_newbcast:5 row_mask:0xf bank_mask:0xf"
+                                 : "+v"(a[i]) : "v"(xs[i & 3]), "v"((i & 4) ? w0 : w1));
+                else
+                    asm volatile("v_fmac_f32_dpp %0, %1, %2 quad_perm:[1,1,1,1] row_mask:0xf bank_mask:0xf bound_ctrl:1"
+                                 : "+v"(a[i]) : "v"(xs[i & 3]), "v"((i & 4) ? w0 : w1));
+            }
+        }
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) s += a[i];
+    out[(int64_t)blockIdx.x * 256 + threadIdx.x] = s;
+}
+
 }  // namespace
+
+extern "C" int rg_probe_fma(int32_t mode, int32_t chains, float* out, int32_t grid, int32_t iters, void* stream) {
+    if (!out || ((uintptr_t)out & 3) || grid < 1 || grid > 65536 || iters < 1 || mode < 0 || mode > 2) return 1;
+    if (chains != 8 && chains != 16) return 1;
+    (void)hipGetLastError();
+    const dim3 g((unsigned)grid), b(256);
+    hipStream_t st = (hipStream_t)stream;
+    switch (mode * 100 + chains) {
+        case 8: hipLaunchKernelGGL((fma_kernel<8, 0>), g, b, 0, st, out, iters); break;
+        case 16: hipLaunchKernelGGL((fma_kernel<16, 0>), g, b, 0, st, out, iters); break;
+        case 108: hipLaunchKernelGGL((fma_kernel<8, 1>), g, b, 0, st, out, iters); break;
+        case 116: hipLaunchKernelGGL((fma_kernel<16, 1>), g, b, 0, st, out, iters); break;
+        case 208: hipLaunchKernelGGL((fma_kernel<8, 2>), g, b, 0, st, out, iters); break;
+        default: hipLaunchKernelGGL((fma_kernel<16, 2>), g, b, 0, st, out, iters); break;
+    }
+    return hipGetLastError() == hipSuccess ? 0 : 4;
+}
 
 extern "C" int rg_probe_read(const void* src, int64_t bytes, uint32_t* sink, int32_t grid, void* stream) {
     if (!src || !sink || bytes < kPiece || bytes % kPiece != 0 || grid < 1 || grid > 65536) return 1;
