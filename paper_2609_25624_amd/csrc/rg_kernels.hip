@@ -2219,14 +2219,7 @@ hipError_t launch_stream(const StreamArgs& a, bool f32_weights, int mt, int grid
 
 template <int MT, int SPW, int DEPTH>
 static hipError_t launch_skinny_t(const SkinnyArgs& a, int nw, hipStream_t stream) {
-    const size_t dyn = skinny_lds_bytes(MT, nw, DEPTH, a.JP);
-    static bool attr = false;   // raise the dynamic-LDS limit once per build of the kernel
-    if (!attr) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<MT, SPW, DEPTH>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-        if (e != hipSuccess) return e;
-        attr = true;
-    }
+    const size_t dyn = skinny_lds_bytes(MT, nw, DEPTH, a.JP);   // up to the CU's 160 KB, no opt-in needed
     const int64_t blocks = (a.groups + 7) / 8 * 8 * a.mslices;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL((skinny_kernel<MT, SPW, DEPTH>), dim3((unsigned)blocks), dim3(nw * 64), dyn, stream, a);
