@@ -293,6 +293,7 @@ bool skinny_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan
         }
     }
     if (best_depth == 0) return false;
+    if (ceil_div(RG, best_g) * 4 * spw > 0x7fffffff) return false;   // steps per wave fit int32
     p->mt = mt;
     p->rq = 4;                 // reported as 16 W rows per row group
     p->tile_m = mt;            // reported: rows of x per slice x W rows per group
