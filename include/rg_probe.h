@@ -4,8 +4,9 @@
  * The linear layer at batch 1 is bound by reading the weights from HBM.  This
  * library holds one kernel that reads a buffer and does nothing else, in the
  * access pattern that measured fastest on MI355X (every wave reads whole 8 KB
- * pieces with 16-byte vector loads, consecutive pieces on consecutive waves, so
- * that at any moment the grid reads one compact window of memory).  Its time
+ * pieces with 16-byte non-temporal vector loads, consecutive pieces on
+ * consecutive waves, so that at any moment the grid reads one compact window
+ * of memory).  Its time
  * over a layer's weight bytes is the floor the layer's kernels are held against
  * (the benchmark's --floors mode).  It is not part of the product path.
  *

@@ -65,6 +65,18 @@ struct WVec<float> {
     }
 };
 
+// A 16-byte load marked non-temporal: for weights that are read once (the caches need
+// not keep them, and x, which every workgroup reads, stays resident).
+template <typename V>
+__device__ __forceinline__ V load_nt(const V* p) {
+    static_assert(sizeof(V) == 16, "16-byte vector");
+    using E = __attribute__((ext_vector_type(4))) uint32_t;
+    const E e = __builtin_nontemporal_load(reinterpret_cast<const E*>(p));
+    V v;
+    __builtin_memcpy(&v, &e, sizeof v);
+    return v;
+}
+
 // Broadcast lane E of every quad (4 lanes) to the whole quad (DPP quad_perm).
 template <int E>
 __device__ __forceinline__ float quad_bcast(float v) {
@@ -125,53 +137,68 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // instruction issues) is saved and restored around it.  On this generation an
 // LDS DMA must not read M0 in the cycle after a scalar write of M0 (one wait
 // state, which the compiler inserts for its own DMA but cannot see inside
-// inline asm): the s_nop provides it.
+// inline asm): the s_nop provides it.  NT: the weight stream, whose bytes are
+// read once, is loaded non-temporal (the caches need not keep it, and x, which
+// every workgroup reads, stays resident); x itself is loaded normally.
+template <bool NT = false>
 __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
     uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %2\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %1, %3\n\t"
-        "s_mov_b32 m0, %0\n\t"
-        : "=&s"(saved)
-        : "v"(voff), "s"(lds_base), "s"(sbase)
-        : "memory");
+    if constexpr (NT) {
+        asm volatile(
+            "s_mov_b32 %0, m0\n\t"
+            "s_mov_b32 m0, %2\n\t"
+            "s_nop 0\n\t"
+            "global_load_lds_dwordx4 %1, %3 nt\n\t"
+            "s_mov_b32 m0, %0\n\t"
+            : "=&s"(saved)
+            : "v"(voff), "s"(lds_base), "s"(sbase)
+            : "memory");
+    } else {
+        asm volatile(
+            "s_mov_b32 %0, m0\n\t"
+            "s_mov_b32 m0, %2\n\t"
+            "s_nop 0\n\t"
+            "global_load_lds_dwordx4 %1, %3\n\t"
+            "s_mov_b32 m0, %0\n\t"
+            : "=&s"(saved)
+            : "v"(voff), "s"(lds_base), "s"(sbase)
+            : "memory");
+    }
 }
 
 // Eight DMA instructions into LDS [lds_base + 1024 t, + 1024), t = 0..7, from
 // sbase + vo[t]: the skinny kernel's step with no clamping (whole row group, whole
 // segments), with no vector instruction spent on addresses (vo[] is loop-invariant).
-// Same M0 handling as dma16.  (The instruction's immediate offset is not used: it
-// would move the LDS destination as well.)
+// Same M0 handling as dma16; non-temporal, as the weight stream.  (The instruction's
+// immediate offset is not used: it would move the LDS destination as well.)
 __device__ __forceinline__ void dma8(const void* sbase, const uint32_t (&vo)[8], uint32_t lds_base) {
     uint32_t saved;
     asm volatile(
         "s_mov_b32 %0, m0\n\t"
         "s_mov_b32 m0, %9\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %1, %10\n\t"
+        "global_load_lds_dwordx4 %1, %10 nt\n\t"
         "s_add_u32 m0, m0, 0x400\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %2, %10\n\t"
+        "global_load_lds_dwordx4 %2, %10 nt\n\t"
         "s_add_u32 m0, m0, 0x400\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %3, %10\n\t"
+        "global_load_lds_dwordx4 %3, %10 nt\n\t"
         "s_add_u32 m0, m0, 0x400\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %4, %10\n\t"
+        "global_load_lds_dwordx4 %4, %10 nt\n\t"
         "s_add_u32 m0, m0, 0x400\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %5, %10\n\t"
+        "global_load_lds_dwordx4 %5, %10 nt\n\t"
         "s_add_u32 m0, m0, 0x400\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %6, %10\n\t"
+        "global_load_lds_dwordx4 %6, %10 nt\n\t"
         "s_add_u32 m0, m0, 0x400\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %7, %10\n\t"
+        "global_load_lds_dwordx4 %7, %10 nt\n\t"
         "s_add_u32 m0, m0, 0x400\n\t"
         "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %8, %10\n\t"
+        "global_load_lds_dwordx4 %8, %10 nt\n\t"
         "s_mov_b32 m0, %0\n\t"
         : "=&s"(saved)
         : "v"(vo[0]), "v"(vo[1]), "v"(vo[2]), "v"(vo[3]), "v"(vo[4]), "v"(vo[5]), "v"(vo[6]), "v"(vo[7]),
@@ -501,7 +528,7 @@ __global__ void __launch_bounds__(NW * 64, 1) decode_kernel(DecodeArgs a) {
             uint32_t col = dma_col[i] + (uint32_t)(s * kSlab * 2);
             if (s * kSlab + dma_kin[i] >= dma_jlen[i]) col = 0;   // past the end of a short last segment
             const uint32_t voff = (uint32_t)(row * row_bytes) + col;
-            dma16(base, voff, slot + 1024u * i);
+            dma16<true>(base, voff, slot + 1024u * i);
         }
     };
 
@@ -743,7 +770,7 @@ __global__ void __launch_bounds__(NW * 64, 1) decode1_kernel(DecodeArgs a) {
             uint32_t col = dma_col[i] + (uint32_t)(s * kSlab * 2);
             if (s * kSlab + dma_kin[i] >= dma_jlen[i]) col = 0;
             const uint32_t voff = (uint32_t)(row * row_bytes) + col;
-            dma16(base, voff, slot + 1024u * i);
+            dma16<true>(base, voff, slot + 1024u * i);
         }
         const uint32_t xslot = xring_base + (uint32_t)((st % DEPTH) * kXSlabBytesPerWave);
 #pragma unroll
@@ -1094,6 +1121,8 @@ __global__ void __launch_bounds__(NT) ktile_kernel(const float* __restrict__ x, 
             const int row = idx / WPR, kh = idx % WPR;
             const int64_t gn = n0 + row, gk = k0 + WE * kh;
             const bool ok = idx < BN * WPR && j < J && gn < N && gk + WE <= K;
+            // (a normal load: a slab reads 16 or 32 bytes of each 128-byte line of a row and the
+            // next slab the rest, which a non-temporal load would not find in the cache)
             wr[u] = ok ? *reinterpret_cast<const typename WV::V*>(w + gn * K + gk) : WV::zero();
         }
     };
@@ -1304,7 +1333,7 @@ __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
 #pragma unroll
             for (int q = 0; q < 4; ++q)
 #pragma unroll
-                for (int m = 0; m < 8; ++m) dma16(base, doff[m] + 128u * q, wbase + 1024u * (8 * q + m));
+                for (int m = 0; m < 8; ++m) dma16<true>(base, doff[m] + 128u * q, wbase + 1024u * (8 * q + m));
         } else {
             // a short last quad or step: absent rows and segments re-read present ones
             // (the same lines as other lanes of the instruction or an earlier one)
@@ -1318,7 +1347,7 @@ __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
                     const int u = (lane & 7) ^ ((c >> 1) & 7);
                     const int r = min(c & 3, rlim), j = min(c >> 2, jlim);
                     const uint32_t voff = (uint32_t)(r * row_bytes) + 512u * (uint32_t)j + 16u * (uint32_t)(8 * q + u);
-                    dma16(base, voff, wbase + 1024u * (8 * q + m));
+                    dma16<true>(base, voff, wbase + 1024u * (8 * q + m));
                 }
         }
     };
@@ -1722,7 +1751,7 @@ __global__ void __launch_bounds__(512) skinny_kernel(SkinnyArgs a) {
             int e = 64 * s + 8 * ((t & 1) ? u1 : u0);
             if (e >= jlen) e = 0;                         // past a short last segment: never read
             const uint32_t voff = (uint32_t)(row * row_bytes) + (uint32_t)(j * (2 * kChunk) + 2 * e);
-            dma16(base, voff, slot + 1024u * t);
+            dma16<true>(base, voff, slot + 1024u * t);
         }
     };
 
@@ -1881,7 +1910,7 @@ __global__ void __launch_bounds__(256) stream_kernel(StreamArgs a) {
 #pragma unroll
         for (int r = 0; r < kStreamRows; ++r) {
             const int64_t n = rb * kStreamRows + r;
-            wr[r] = (n < N && k0 + e0 < K) ? *reinterpret_cast<const typename WV::V*>(w + n * K + k0 + e0)
+            wr[r] = (n < N && k0 + e0 < K) ? load_nt(reinterpret_cast<const typename WV::V*>(w + n * K + k0 + e0))
                                            : WV::zero();
         }
 #pragma unroll

@@ -9,6 +9,13 @@ namespace {
 constexpr int kPiece = 8192;                 // bytes per wave piece: 8 loads of 1 KB per wave
 constexpr int kLoads = kPiece / (64 * 16);   // 16-byte loads per lane per piece
 
+// One 16-byte load, non-temporal (data read once; the linear-layer kernels stream weights so).
+__device__ __forceinline__ uint4 ld(const uint4* p) {
+    using E = __attribute__((ext_vector_type(4))) uint32_t;
+    const E e = __builtin_nontemporal_load(reinterpret_cast<const E*>(p));
+    return make_uint4(e.x, e.y, e.z, e.w);
+}
+
 // Wave v of W reads pieces v, v + W, v + 2W, ... two at a time (16 loads in flight per lane).
 __global__ void __launch_bounds__(256) read_kernel(const uint4* __restrict__ src, int64_t pieces, uint32_t* sink) {
     const int lane = threadIdx.x & 63;
@@ -21,9 +28,9 @@ __global__ void __launch_bounds__(256) read_kernel(const uint4* __restrict__ src
         const uint4* pa = src + p * (kPiece / 16) + lane;
         const uint4* pb = src + (p + waves) * (kPiece / 16) + lane;
 #pragma unroll
-        for (int i = 0; i < kLoads; ++i) a[i] = pa[64 * i];
+        for (int i = 0; i < kLoads; ++i) a[i] = ld(pa + 64 * i);
 #pragma unroll
-        for (int i = 0; i < kLoads; ++i) b[i] = pb[64 * i];
+        for (int i = 0; i < kLoads; ++i) b[i] = ld(pb + 64 * i);
 #pragma unroll
         for (int i = 0; i < kLoads; ++i) acc ^= a[i].x ^ a[i].y ^ a[i].z ^ a[i].w ^ b[i].x ^ b[i].y ^ b[i].z ^ b[i].w;
     }
@@ -31,7 +38,7 @@ __global__ void __launch_bounds__(256) read_kernel(const uint4* __restrict__ src
         const uint4* pa = src + p * (kPiece / 16) + lane;
 #pragma unroll
         for (int i = 0; i < kLoads; ++i) {
-            const uint4 a = pa[64 * i];
+            const uint4 a = ld(pa + 64 * i);
             acc ^= a.x ^ a.y ^ a.z ^ a.w;
         }
     }
