@@ -32,6 +32,14 @@
 #include "rg_kernels.h"
 
 namespace rg {
+
+// A 16-byte non-temporal load (key and value rows that a pass reads whole, once per call).
+__device__ __forceinline__ uint4 ldnt(const uint4* p) {
+    using E = __attribute__((ext_vector_type(4))) uint32_t;
+    const E e = __builtin_nontemporal_load(reinterpret_cast<const E*>(p));
+    return make_uint4(e.x, e.y, e.z, e.w);
+}
+
 namespace {
 
 constexpr int kAttnSeg = 256;                 // positions per segment
@@ -82,7 +90,7 @@ struct Tile {
         for (int u = 0; u < NV; ++u) {
             const int i = (int)threadIdx.x + 256 * u;
             const int row = row_of(i, vpr, vmagic);
-            r[u] = i < limit ? *reinterpret_cast<const uint4*>(src + row * stride + 8 * (i - row * vpr))
+            r[u] = i < limit ? ldnt(reinterpret_cast<const uint4*>(src + row * stride + 8 * (i - row * vpr)))
                              : make_uint4(0u, 0u, 0u, 0u);
         }
     }
@@ -248,6 +256,8 @@ __global__ void __launch_bounds__(128) attn_scores2_kernel(AttnArgs a) {
         for (int u = 0; u < NV; ++u) {
             const int i = tid + 128 * u;               // vector i: row i / 4, columns 8 (i % 4)
             const int row = i >> 2;
+            // a normal load: each pass reads 64 bytes of a row whose other bytes the next
+            // passes read (non-temporal here measured slower on the 70B-shaped heads)
             kr[u] = row < w.rows ? *reinterpret_cast<const uint4*>(src + (int64_t)row * D + 8 * (i & 3))
                                  : make_uint4(0u, 0u, 0u, 0u);
         }
@@ -525,7 +535,7 @@ __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
         for (int u = 0; u < NVL; ++u) {
             const int i = lane + 64 * u;                // vector i: row i / (D / 8), column 8 (i % (D / 8))
             const int row = i / (D / 8);
-            vr[u] = row < nrow ? *reinterpret_cast<const uint4*>(vb + (int64_t)row * D + 8 * (i % (D / 8)))
+            vr[u] = row < nrow ? ldnt(reinterpret_cast<const uint4*>(vb + (int64_t)row * D + 8 * (i % (D / 8))))
                                : make_uint4(0u, 0u, 0u, 0u);
         }
         const int64_t tb = ((int64_t)w.b * a.H + (int64_t)w.g * G) * a.Lmax + w.l0 + r0;
