@@ -169,41 +169,31 @@ __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t
 // Eight DMA instructions into LDS [lds_base + 1024 t, + 1024), t = 0..7, from
 // sbase + vo[t]: the skinny kernel's step with no clamping (whole row group, whole
 // segments), with no vector instruction spent on addresses (vo[] is loop-invariant).
-// Same M0 handling as dma16; non-temporal, as the weight stream.  (The instruction's
-// immediate offset is not used: it would move the LDS destination as well.)
+// Same M0 handling as dma16; NT as there.  (The instruction's immediate offset is
+// not used: it would move the LDS destination as well.)
+template <bool NT>
 __device__ __forceinline__ void dma8(const void* sbase, const uint32_t (&vo)[8], uint32_t lds_base) {
+#define RG_DMA8(P)                                                                                          \
+    asm volatile("s_mov_b32 %0, m0\n\t"                                                                    \
+                 "s_mov_b32 m0, %9\n\t"                                                                    \
+                 "s_nop 0\n\t"                                                                             \
+                 "global_load_lds_dwordx4 %1, %10" P "\n\t"                                                 \
+                 "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %10" P "\n\t"         \
+                 "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %3, %10" P "\n\t"         \
+                 "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %4, %10" P "\n\t"         \
+                 "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %5, %10" P "\n\t"         \
+                 "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %6, %10" P "\n\t"         \
+                 "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %7, %10" P "\n\t"         \
+                 "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %8, %10" P "\n\t"         \
+                 "s_mov_b32 m0, %0\n\t"                                                                    \
+                 : "=&s"(saved)                                                                             \
+                 : "v"(vo[0]), "v"(vo[1]), "v"(vo[2]), "v"(vo[3]), "v"(vo[4]), "v"(vo[5]), "v"(vo[6]),     \
+                   "v"(vo[7]), "s"(lds_base), "s"(sbase)                                                    \
+                 : "memory", "scc")
     uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %9\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %1, %10 nt\n\t"
-        "s_add_u32 m0, m0, 0x400\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %2, %10 nt\n\t"
-        "s_add_u32 m0, m0, 0x400\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %3, %10 nt\n\t"
-        "s_add_u32 m0, m0, 0x400\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %4, %10 nt\n\t"
-        "s_add_u32 m0, m0, 0x400\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %5, %10 nt\n\t"
-        "s_add_u32 m0, m0, 0x400\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %6, %10 nt\n\t"
-        "s_add_u32 m0, m0, 0x400\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %7, %10 nt\n\t"
-        "s_add_u32 m0, m0, 0x400\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %8, %10 nt\n\t"
-        "s_mov_b32 m0, %0\n\t"
-        : "=&s"(saved)
-        : "v"(vo[0]), "v"(vo[1]), "v"(vo[2]), "v"(vo[3]), "v"(vo[4]), "v"(vo[5]), "v"(vo[6]), "v"(vo[7]),
-          "s"(lds_base), "s"(sbase)
-        : "memory", "scc");
+    if constexpr (NT) RG_DMA8(" nt");
+    else RG_DMA8("");
+#undef RG_DMA8
 }
 
 // Wait until at most N vector-memory operations of this wave are outstanding.
@@ -1731,6 +1721,9 @@ __global__ void __launch_bounds__(512) skinny_kernel(SkinnyArgs a) {
 #pragma unroll
     for (int t = 0; t < 8; ++t)
         vo[t] = (uint32_t)(((t & 1) ? ic1 : ic0) * row_bytes) + 512u * (t >> 1) + 16u * ((t & 1) ? u1 : u0);
+    // one slice: the weights are read once, non-temporal; several slices read each row group
+    // once per slice, the later ones from L2, so it is kept there
+    const bool nt = a.mslices == 1;
     auto issue = [&](int st) {
         const int r = st / tpr;
         const int qs = st - r * tpr;
@@ -1740,7 +1733,9 @@ __global__ void __launch_bounds__(512) skinny_kernel(SkinnyArgs a) {
         const int rmax = (int)min((int64_t)15, N - 1 - n0);
         const uint32_t slot = ring_base + (uint32_t)((st % DEPTH) * kSkSlabBytes);
         if (rmax == 15 && (4 * sg + 4 < J || (4 * sg + 4 == J && last_len == kChunk))) {
-            dma8(base + (int64_t)(4 * sg * kChunk + 64 * s) * 2, vo, slot);
+            const char* sb = base + (int64_t)(4 * sg * kChunk + 64 * s) * 2;
+            if (nt) dma8<true>(sb, vo, slot);
+            else dma8<false>(sb, vo, slot);
             return;
         }
 #pragma unroll
@@ -1751,7 +1746,8 @@ __global__ void __launch_bounds__(512) skinny_kernel(SkinnyArgs a) {
             int e = 64 * s + 8 * ((t & 1) ? u1 : u0);
             if (e >= jlen) e = 0;                         // past a short last segment: never read
             const uint32_t voff = (uint32_t)(row * row_bytes) + (uint32_t)(j * (2 * kChunk) + 2 * e);
-            dma16<true>(base, voff, slot + 1024u * t);
+            if (nt) dma16<true>(base, voff, slot + 1024u * t);
+            else dma16<false>(base, voff, slot + 1024u * t);
         }
     };
 
