@@ -74,15 +74,17 @@ typedef enum {
     RG_KERNEL_GENERIC = 0,   /* one thread per output; any K, any alignment */
     RG_KERNEL_DECODE = 1,    /* M <= 4 (or K < 4096 up to M = 64): streaming skinny GEMM, x in registers */
     RG_KERNEL_TILED = 2,     /* larger M: register-tiled kernel, whole K per workgroup */
-    RG_KERNEL_DECODE_XS = 3, /* M == 1: streaming GEMV with x streamed through LDS beside W */
-    RG_KERNEL_GEMV = 4,      /* M == 1, K % 256 == 0, K >= 4096: 32 KB W bursts, whole rows per wave */
+    RG_KERNEL_DECODE_XS = 3, /* M == 1 (when forced, or where the skinny kernel's x does not fit its
+                                registers): streaming GEMV with x streamed through LDS beside W */
+    RG_KERNEL_GEMV = 4,      /* M == 1, K % 256 == 0, K >= 4096 (when forced, or where the skinny
+                                kernel's x does not fit): 32 KB W bursts, whole rows per wave */
     RG_KERNEL_STREAM = 5,    /* M <= 4: 8-row blocks of W streamed through LDS, one chain per lane
                                 (FP32 weights by default; BF16 weights when forced) */
     RG_KERNEL_KTILE = 6,     /* 16 < M <= 64 (any M when forced): 4 x 4 register tiles, K segments
                                 shared out over thread groups */
-    RG_KERNEL_SKINNY = 7     /* 2 <= M <= 16: waves of 16 W rows x 4 segments, x of a segment
-                                shared by 16 lanes through DPP row broadcasts, slices of 2, 4 or
-                                8 rows of x */
+    RG_KERNEL_SKINNY = 7     /* M <= 16: waves of 16 W rows x 4 segments, x of a segment shared
+                                by 16 lanes through DPP row broadcasts, slices of 1, 2, 4 or 8
+                                rows of x */
 } rg_kernel_id;
 
 /* Scheduling overrides for the determinism tests.  0 in a field = planner

@@ -230,7 +230,7 @@ bool ktile_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan*
     return true;
 }
 
-// Skinny kernel: slices of mt = 2, 4 or 8 rows of x, waves of 16 W rows x 4 segments with
+// Skinny kernel: slices of mt = 1, 2, 4 or 8 rows of x, waves of 16 W rows x 4 segments with
 // x shared through DPP row broadcasts.  Each wave keeps x of spw segment groups in registers
 // (16 * mt * spw <= 128 floats), so nw = ceil(NSG / spw) <= 8 waves cover K.  Two waves per
 // SIMD: ceil(8 / nw) workgroups per CU where LDS allows.  Depth (steps in flight per wave):
@@ -239,7 +239,7 @@ constexpr int64_t kSkinnyMaxM = 16;
 constexpr int64_t kLdsBytes = 160 * 1024;
 
 bool skinny_shape_ok(int64_t M, int64_t K) {
-    return M >= 2 && K < ((int64_t)1 << 26);
+    return M >= 1 && K < ((int64_t)1 << 26);
 }
 
 bool skinny_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan* p) {
@@ -257,7 +257,7 @@ bool skinny_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan
     }
     if (spw == 3) spw = 4;
     // the widest slice whose x registers fit (narrower slices read W once more each, mostly from L2)
-    int mt = M <= 2 ? 2 : (M <= 4 ? 4 : 8);
+    int mt = M <= 1 ? 1 : (M <= 2 ? 2 : (M <= 4 ? 4 : 8));
     while (mt > 2 && mt * spw > 8) mt /= 2;
     if (spw > 4 || mt * spw > 8) return false;
     const int64_t S = ceil_div(M, mt);
@@ -406,16 +406,18 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     const bool decode_ok = fast_ok && J <= 112 && mslices <= 65536;
     const bool tiled_ok = fast_ok;
     const bool gemv_ok = fast_ok && M == 1 && gemv_shape_ok(N, K);
-    // M == 1: the 32 KB-burst kernel where one step covers K (J == 16); the
-    // slab-streaming kernels elsewhere (they measure faster once x must be
-    // re-read from LDS every step)
+    // M == 1 where the skinny schedule does not fit: the 32 KB-burst kernel where one
+    // step covers K (J == 16); the slab-streaming kernels elsewhere (they measure faster
+    // once x must be re-read from LDS every step)
     const bool ktile_ok = fast_ok && M <= kDecodeMaxM;
     // ktile from M = 9 on; for 5 <= M <= 8 only where its 16 x 16 tiles are many (measured:
     // the streaming decode kernel is faster on the narrow layers there)
     const bool ktile_pref = M > 8 || (M > 4 && ceil_div(N, 16) >= 384);
     const bool skinny_ok = fast_ok && skinny_shape_ok(M, K);
-    if (gemv_ok && ceil_div(K, rg::kChunk) == 16) want = RG_KERNEL_GEMV;
-    else if (skinny_ok && M <= kSkinnyMaxM) want = RG_KERNEL_SKINNY;
+    // M == 1 too: the one-row skinny build measured 2 % faster than the GEMV on the
+    // 28672 x 4096, 4096 x 14336 and 128256 x 4096 layers and level on the two narrow ones
+    if (skinny_ok && M <= kSkinnyMaxM) want = RG_KERNEL_SKINNY;
+    else if (gemv_ok && ceil_div(K, rg::kChunk) == 16) want = RG_KERNEL_GEMV;
     else if (ktile_ok && ktile_pref) want = RG_KERNEL_KTILE;
     else if (decode_ok && M <= kDecodeMaxM) want = (M == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;
     else if (tiled_ok) want = RG_KERNEL_TILED;
@@ -438,8 +440,12 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         if (forced || o.waves_per_wg > 0 || o.grid_wgs > 0 || o.depth > 0) return RG_ERR_RANGE;
         // x of a wave's segment groups does not fit its registers: the earlier kernels
         p->mslices = 1;
-        want = p->kernel = (ktile_ok && ktile_pref) ? RG_KERNEL_KTILE
-                         : (decode_ok ? RG_KERNEL_DECODE : (tiled_ok ? RG_KERNEL_TILED : RG_KERNEL_GENERIC));
+        if (M == 1)
+            want = p->kernel = (gemv_ok && J == 16) ? RG_KERNEL_GEMV
+                             : (decode_ok ? RG_KERNEL_DECODE_XS : (tiled_ok ? RG_KERNEL_TILED : RG_KERNEL_GENERIC));
+        else
+            want = p->kernel = (ktile_ok && ktile_pref) ? RG_KERNEL_KTILE
+                             : (decode_ok ? RG_KERNEL_DECODE : (tiled_ok ? RG_KERNEL_TILED : RG_KERNEL_GENERIC));
     }
     if (want == RG_KERNEL_KTILE) {
         if (ktile_schedule(M, N, K, o, p)) return RG_OK;

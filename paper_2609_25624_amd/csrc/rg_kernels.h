@@ -52,7 +52,7 @@ struct StreamArgs {
     int reverse;          // reversed workgroup-to-block mapping
 };
 
-// Arguments of the skinny kernel (M >= 2, K % 8 == 0, K < 2^26, x and W 16-byte aligned).
+// Arguments of the skinny kernel (M >= 1, K % 8 == 0, K < 2^26, x and W 16-byte aligned).
 struct SkinnyArgs {
     const float* x;
     const uint16_t* w;

@@ -1538,7 +1538,7 @@ __global__ void __launch_bounds__(NW * 64, 1) gemv_kernel(GemvArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// skinny kernel (2 <= M, K % 8 == 0): x shared by the 16 lanes of a DPP row.
+// skinny kernel (M >= 1, K % 8 == 0): x shared by the 16 lanes of a DPP row.
 //
 // Work split.  W rows come in groups of 16 and K in groups of 4 segments.  A
 // wave works on one (row group, segment group) pair at a time: lane 16d + i
@@ -1591,6 +1591,19 @@ __device__ __forceinline__ void fmac_nb4(float (&acc)[4], const float (&X)[4][16
 #undef RG_G
 }
 
+// the same for one row of x and h = 0..7
+template <int L, int E0>
+__device__ __forceinline__ void fmac_nb1(float (&acc)[1], const float (&X)[1][16], const float* w) {
+#define RG_G(X, W) "v_fmac_f32_dpp %0, %" #X ", %" #W " row_newbcast:%17 row_mask:0xf bank_mask:0xf\n\t"
+    asm("s_nop 1\n\t"
+        RG_G(1, 9) RG_G(2, 10) RG_G(3, 11) RG_G(4, 12) RG_G(5, 13) RG_G(6, 14) RG_G(7, 15) RG_G(8, 16)
+        : "+v"(acc[0])
+        : "v"(X[0][E0]), "v"(X[0][E0 + 1]), "v"(X[0][E0 + 2]), "v"(X[0][E0 + 3]),
+          "v"(X[0][E0 + 4]), "v"(X[0][E0 + 5]), "v"(X[0][E0 + 6]), "v"(X[0][E0 + 7]),
+          "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), "v"(w[4]), "v"(w[5]), "v"(w[6]), "v"(w[7]), "n"(L));
+#undef RG_G
+}
+
 // the same for two rows of x and h = 0..7
 template <int L, int E0>
 __device__ __forceinline__ void fmac_nb2(float (&acc)[2], const float (&X)[2][16], const float* w) {
@@ -1637,7 +1650,9 @@ __device__ __forceinline__ void sk_piece(float (&acc)[MT], const float (&X)[MT][
 #pragma unroll
     for (int h = 0; h < 8; ++h) wv[h] = (h & 1) ? up_hi(d[h >> 1]) : up_lo(d[h >> 1]);
     constexpr int L = 4 * S + T / 2, E0 = 8 * (T & 1);
-    if constexpr (MT == 2) {
+    if constexpr (MT == 1) {
+        fmac_nb1<L, E0>(acc, X, wv);
+    } else if constexpr (MT == 2) {
         fmac_nb2<L, E0>(acc, X, wv);
     } else if constexpr (MT == 4) {
         fmac_nb4<L, E0>(acc, X, wv);
@@ -1666,7 +1681,7 @@ __device__ __forceinline__ void sk_step(float (&acc)[MT], const float (&X)[MT][1
 
 template <int MT, int SPW, int DEPTH>
 __global__ void __launch_bounds__(512) skinny_kernel(SkinnyArgs a) {
-    static_assert(MT == 2 || MT == 4 || MT == 8, "rows of x per slice");
+    static_assert(MT == 1 || MT == 2 || MT == 4 || MT == 8, "rows of x per slice");
     static_assert(SPW >= 1 && MT * SPW <= 8, "x registers: 16 * MT * SPW <= 128");
     static_assert(DEPTH >= 2 && DEPTH <= 3, "ring depth");
     extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];
@@ -2263,6 +2278,9 @@ hipError_t launch_skinny(const SkinnyArgs& a, int mt, int spw, int nw, int depth
     if (nw < 1 || nw > 8 || a.JP < a.J || skinny_lds_bytes(mt, nw, depth, a.JP) > 160 * 1024) return hipErrorInvalidValue;
     if ((int64_t)nw * spw < a.NSG) return hipErrorInvalidValue;   // every segment group has a wave
     switch (mt * 10 + spw) {
+        case 11: return launch_skinny_d<1, 1>(a, nw, depth, stream);
+        case 12: return launch_skinny_d<1, 2>(a, nw, depth, stream);
+        case 14: return launch_skinny_d<1, 4>(a, nw, depth, stream);
         case 21: return launch_skinny_d<2, 1>(a, nw, depth, stream);
         case 22: return launch_skinny_d<2, 2>(a, nw, depth, stream);
         case 24: return launch_skinny_d<2, 4>(a, nw, depth, stream);

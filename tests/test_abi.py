@@ -63,7 +63,7 @@ def test_plan_numeric_fields_depend_on_k_only():
 
 def test_plan_is_pure_and_overrides_are_scheduling_only():
     for shape, ov in (((4, 6144, 4096), (4, 100, 2)), ((1, 6144, 4096), (2, 100, 3))):
-        want = ov if shape[0] > 1 else (ov[0], ov[1], 0)
+        want = ov
         a = rg.rg_plan(*shape)
         assert a == rg.rg_plan(*shape)
         rg.rg_linear_set_launch(waves_per_wg=ov[0], grid_wgs=ov[1], depth=ov[2], grid_order=1)
@@ -100,9 +100,9 @@ def test_gemv_schedule_defaults():
         assert rg.rg_plan(1, 4096, 4096)["waves_per_wg"] == 3
     finally:
         rg.rg_linear_set_launch(None)
-    rg.rg_linear_set_launch(waves_per_wg=4)     # not forced: another kernel takes the shape
+    rg.rg_linear_set_launch(waves_per_wg=4)     # not forced: the planner's kernel takes the override
     try:
-        assert rg.rg_plan(1, 4096, 14336)["kernel_name"] == "decode_xs"
+        assert rg.rg_plan(1, 4096, 14336)["kernel_name"] == "skinny"
     finally:
         rg.rg_linear_set_launch(None)
 

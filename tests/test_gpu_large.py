@@ -24,7 +24,8 @@ def _reset_launch():
     rg.rg_linear_set_launch(None)
 
 
-@pytest.mark.parametrize("M,N,K,kernel,forced", [(1, 1048579, 2304, "decode_xs", False), (1, 524309, 4096, "gemv", False),
+@pytest.mark.parametrize("M,N,K,kernel,forced", [(1, 1048579, 2304, "skinny", False), (1, 524309, 4096, "skinny", False),
+                                                 (1, 1048579, 2304, "decode_xs", True), (1, 524309, 4096, "gemv", True),
                                                  (3, 1048579, 2304, "skinny", False), (16, 1048579, 2304, "skinny", False),
                                                  (3, 1048579, 2304, "decode", True), (16, 1048579, 2304, "ktile", True),
                                                  (70, 1048579, 2304, "tiled", False)])

@@ -1,11 +1,11 @@
-"""The skinny kernel (2 <= M <= 16: 16 W rows x 4 segments per wave, x shared by the 16 lanes
-of a DPP row) against the oracle, bit for bit.
+"""The skinny kernel (M <= 16: 16 W rows x 4 segments per wave, x shared by the 16 lanes of a
+DPP row) against the oracle, bit for bit.
 
 Shapes cover the batched-decode layers of an 8B Llama-3-class model (Supplement A, decode
 latency; Design, the decode bucket of R4), ragged row groups (N % 16 != 0), short last
 segments (K % 256 != 0), segment counts that leave rows of a wave idle (J % 4 != 0), several
 segment groups per wave (J > 32), slices of x (M > 8, or x registers capped), every build
-(rows of x per slice 2, 4, 8; segment groups per wave 1, 2, 4; depth 2, 3) and the
+(rows of x per slice 1, 2, 4, 8; segment groups per wave 1, 2, 4; depth 2, 3) and the
 launch overrides.
 """
 import numpy as np
@@ -52,13 +52,13 @@ def _check(M, N, K, seed=0, cfg=None, expect=None, bias=False):
     gu.assert_bitwise(y.cpu().numpy(), gu.oracle_full(x, w), f"skinny ({M},{N},{K}) {cfg}")
 
 
-@pytest.mark.parametrize("M", [2, 3, 4, 8, 16])
+@pytest.mark.parametrize("M", [1, 2, 3, 4, 8, 16])
 @pytest.mark.parametrize("N,K", [(6144, 4096), (4096, 4096), (28672, 4096), (4096, 14336)])
 def test_llama_decode_layers_full_output(M, N, K):
     _check(M, N, K, seed=M * 7 + K)
 
 
-@pytest.mark.parametrize("M", [2, 4, 5, 9, 16])
+@pytest.mark.parametrize("M", [1, 2, 4, 5, 9, 16])
 @pytest.mark.parametrize("N,K", [(1, 8), (15, 264), (17, 1000), (33, 1280), (130, 2056), (1000, 4104),
                                  (77, 9000), (31, 14336), (19, 28672)])
 def test_ragged_shapes(M, N, K):
@@ -124,3 +124,16 @@ def test_order_probes_inside_rows():
         if x1.shape[1] == K:
             want = int(p["expect_bits"], 16)
             assert int(gu.bits(got)[5, row]) == want, p["name"]
+
+
+@pytest.mark.parametrize("N,K", [(6144, 4096), (4096, 14336), (33, 1280), (17, 1000), (1, 8), (130, 2056)])
+@pytest.mark.parametrize("cfg", [dict(), dict(waves_per_wg=4), dict(depth=3, grid_order=1)])
+def test_one_row_build_overrides(N, K, cfg):
+    """M = 1 through the skinny kernel's one-row build, under launch overrides."""
+    import paper_2609_25624_amd as rg
+    rg.rg_linear_set_launch(kernel="skinny", **cfg)
+    try:
+        rg.rg_plan(1, N, K)
+    except rg.RgError:
+        pytest.skip(f"{cfg} not valid for (1,{N},{K})")
+    _check(1, N, K, seed=N + K, cfg=cfg, expect={"tile_m": 1})
