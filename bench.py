@@ -120,7 +120,8 @@ def run_fma_rates():
     stream = torch.cuda.current_stream()
     out = torch.empty(768 * 256, dtype=torch.float32, device=dev)
     iters = 4096
-    for mode, mname in ((0, "plain"), (1, "dpp_row_newbcast"), (2, "dpp_quad_perm")):
+    for mode, mname in ((0, "plain"), (1, "dpp_row_newbcast"), (2, "dpp_quad_perm"), (3, "sgpr"),
+                        (4, "sgpr_and_plain_in_turn")):
         for chains in (8, 16):
             for grid in (256, 512, 768):
                 probe.rg_probe_fma(mode, chains, out, grid, iters, stream=stream)

@@ -20,7 +20,9 @@
  * ceilings they are held against.  Every thread of grid workgroups of 256 runs
  * `chains` (8 or 16) independent v_fmac_f32 chains for iters * 64 steps, each
  * FMA's first operand read plainly (mode 0), through a DPP row broadcast
- * (mode 1) or a DPP quad broadcast (mode 2), the forms the kernels use; 2 * 64 *
+ * (mode 1), through a DPP quad broadcast (mode 2), from an SGPR shared by the
+ * wave (mode 3), or from an SGPR and a plain VGPR in turn (mode 4), the forms
+ * the kernels use; 2 * 64 *
  * iters * grid * 256 flops per launch.  out: device pointer to grid * 256
  * floats (the chains' sums).  Returns 0, 1 on an invalid argument, 4 on a
  * launch error.

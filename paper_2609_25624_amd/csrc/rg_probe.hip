@@ -47,8 +47,9 @@ __global__ void __launch_bounds__(256) read_kernel(const uint4* __restrict__ src
 
 // FMA issue-rate probe: CH independent accumulator chains per thread, each step one
 // v_fmac_f32 per chain with its first operand read plainly (MODE 0), through a DPP row
-// broadcast (MODE 1, row_newbcast) or a DPP quad broadcast (MODE 2, quad_perm), as the
-// linear-layer kernels use them.  The operands are non-trivial values near 1 (so the
+// broadcast (MODE 1, row_newbcast), through a DPP quad broadcast (MODE 2, quad_perm), from
+// an SGPR (MODE 3, a value the whole wave shares; a different SGPR for each chain) or from an
+// SGPR and a VGPR in turn (MODE 4: even chains SGPR, odd chains plain).  The operands are non-trivial values near 1 (so the
 // arithmetic switches as much as real data does).
 template <int CH, int MODE>
 __global__ void __launch_bounds__(256) fma_kernel(float* out, int iters) {
@@ -57,10 +58,17 @@ __global__ void __launch_bounds__(256) fma_kernel(float* out, int iters) {
     for (int i = 0; i < CH; ++i) a[i] = threadIdx.x * 1e-3f + i;
     const float xs[4] = {1.0001f + threadIdx.x * 1e-9f, 0.9999f, 1.00002f, 0.99998f};
     const float w0 = 0.5f + threadIdx.x * 1e-7f, w1 = 0.25f;
+    // wave-uniform operands, held in SGPRs (the empty asm keeps each in its own SGPR)
+    int sx[CH];
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+        sx[j] = __builtin_amdgcn_readfirstlane(__float_as_int(xs[j & 3]) + j * 7);
+        if constexpr (MODE >= 3) asm volatile("" : "+s"(sx[j]));
+    }
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
         for (int r = 0; r < 64 / CH; ++r) {
-            if (MODE != 0) asm volatile("s_nop 1");   // the wait states a DPP read of a fresh VGPR needs
+            if (MODE == 1 || MODE == 2) asm volatile("s_nop 1");   // the wait states a DPP read of a fresh VGPR needs
 #pragma unroll
             for (int i = 0; i < CH; ++i) {
                 if constexpr (MODE == 0)
@@ -68,9 +76,15 @@ __global__ void __launch_bounds__(256) fma_kernel(float* out, int iters) {
                 else if constexpr (MODE == 1)
                     asm volatile("v_fmac_f32_dpp %0, %1, %2 row_newbcast:5 row_mask:0xf bank_mask:0xf"
                                  : "+v"(a[i]) : "v"(xs[i & 3]), "v"((i & 4) ? w0 : w1));
-                else
+                else if constexpr (MODE == 2)
                     asm volatile("v_fmac_f32_dpp %0, %1, %2 quad_perm:[1,1,1,1] row_mask:0xf bank_mask:0xf bound_ctrl:1"
                                  : "+v"(a[i]) : "v"(xs[i & 3]), "v"((i & 4) ? w0 : w1));
+                else if constexpr (MODE == 3)
+                    asm volatile("v_fmac_f32 %0, %1, %2" : "+v"(a[i]) : "s"(sx[i]), "v"((i & 4) ? w0 : w1));
+                else if (i & 1)
+                    asm volatile("v_fmac_f32 %0, %1, %2" : "+v"(a[i]) : "v"(xs[i & 3]), "v"((i & 4) ? w0 : w1));
+                else
+                    asm volatile("v_fmac_f32 %0, %1, %2" : "+v"(a[i]) : "s"(sx[i]), "v"((i & 4) ? w0 : w1));
             }
         }
     }
@@ -83,7 +97,7 @@ __global__ void __launch_bounds__(256) fma_kernel(float* out, int iters) {
 }  // namespace
 
 extern "C" int rg_probe_fma(int32_t mode, int32_t chains, float* out, int32_t grid, int32_t iters, void* stream) {
-    if (!out || ((uintptr_t)out & 3) || grid < 1 || grid > 65536 || iters < 1 || mode < 0 || mode > 2) return 1;
+    if (!out || ((uintptr_t)out & 3) || grid < 1 || grid > 65536 || iters < 1 || mode < 0 || mode > 4) return 1;
     if (chains != 8 && chains != 16) return 1;
     (void)hipGetLastError();
     const dim3 g((unsigned)grid), b(256);
@@ -94,7 +108,11 @@ extern "C" int rg_probe_fma(int32_t mode, int32_t chains, float* out, int32_t gr
         case 108: hipLaunchKernelGGL((fma_kernel<8, 1>), g, b, 0, st, out, iters); break;
         case 116: hipLaunchKernelGGL((fma_kernel<16, 1>), g, b, 0, st, out, iters); break;
         case 208: hipLaunchKernelGGL((fma_kernel<8, 2>), g, b, 0, st, out, iters); break;
-        default: hipLaunchKernelGGL((fma_kernel<16, 2>), g, b, 0, st, out, iters); break;
+        case 216: hipLaunchKernelGGL((fma_kernel<16, 2>), g, b, 0, st, out, iters); break;
+        case 308: hipLaunchKernelGGL((fma_kernel<8, 3>), g, b, 0, st, out, iters); break;
+        case 316: hipLaunchKernelGGL((fma_kernel<16, 3>), g, b, 0, st, out, iters); break;
+        case 408: hipLaunchKernelGGL((fma_kernel<8, 4>), g, b, 0, st, out, iters); break;
+        default: hipLaunchKernelGGL((fma_kernel<16, 4>), g, b, 0, st, out, iters); break;
     }
     return hipGetLastError() == hipSuccess ? 0 : 4;
 }

@@ -38,7 +38,8 @@ def rg_probe_read(src, sink, grid, stream=None):
 
 
 def rg_probe_fma(mode, chains, out, grid, iters, stream=None):
-    """FMA issue-rate probe (mode 0 plain, 1 DPP row broadcast, 2 DPP quad broadcast); out: float32 [grid * 256]."""
+    """FMA issue-rate probe (mode 0 plain, 1 DPP row broadcast, 2 DPP quad broadcast, 3 SGPR operand,
+    4 SGPR and plain operands in turn); out: float32 [grid * 256]."""
     import torch
     if not (isinstance(out, torch.Tensor) and out.is_cuda and out.dtype == torch.float32 and out.numel() >= grid * 256):
         raise ValueError("out must be a float32 device tensor of grid * 256 elements")

@@ -365,7 +365,7 @@ def test_probe_library_exports_and_host_checks():
     assert L.rg_probe_read(0x1008, 8192, 0x2000, 1, None) == 1          # misaligned
     assert L.rg_probe_read(0x1000, 8192, 0x2000, 0, None) == 1          # no workgroups
     assert L.rg_probe_fma(0, 8, None, 1, 1, None) == 1
-    assert L.rg_probe_fma(3, 8, 0x1000, 1, 1, None) == 1                # no such mode
+    assert L.rg_probe_fma(5, 8, 0x1000, 1, 1, None) == 1                # no such mode
     assert L.rg_probe_fma(0, 12, 0x1000, 1, 1, None) == 1               # 8 or 16 chains
     assert L.rg_probe_fma(0, 8, 0x1000, 0, 1, None) == 1
     assert L.rg_probe_fma(0, 8, 0x1000, 1, 0, None) == 1
