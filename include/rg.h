@@ -103,6 +103,9 @@ typedef enum {
  *                   skinny: 8 KB steps in flight per wave
  *   grid_order    : 0 = forward, 1 = reversed workgroup-to-rows mapping
  *   tile_n        : 0 = planner default, else 16, 32 or 64: ktile's W rows per tile
+ *   slice_m       : 0 = planner default, else 1, 2, 4 or 8: skinny's rows of x per slice
+ *                   (M > slice_m runs ceil(M / slice_m) slices, each streaming all of W;
+ *                    capped at what the kernel's x registers hold)
  *   reserved      : must be 0
  */
 typedef struct {
@@ -112,7 +115,8 @@ typedef struct {
     int32_t depth;
     int32_t grid_order;
     int32_t tile_n;
-    int32_t reserved[2];
+    int32_t slice_m;
+    int32_t reserved;
 } rg_launch_t;
 
 /* What rg_linear will do for a shape (on a 256-CU MI355X with default launch). */

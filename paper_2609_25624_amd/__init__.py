@@ -28,7 +28,7 @@ class RgError(RuntimeError):
 class rg_launch_t(ctypes.Structure):
     _fields_ = [("kernel", ctypes.c_int32), ("waves_per_wg", ctypes.c_int32), ("grid_wgs", ctypes.c_int32),
                 ("depth", ctypes.c_int32), ("grid_order", ctypes.c_int32), ("tile_n", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 2)]
+                ("slice_m", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class rg_plan_t(ctypes.Structure):
@@ -176,7 +176,7 @@ def rg_linear_ptr(x_ptr, w_ptr, y_ptr, M, N, K, stream_ptr=0):
 
 
 def rg_linear_set_launch(cfg=None, **kw):
-    """Scheduling overrides (kernel, waves_per_wg, grid_wgs, depth, grid_order, tile_n); None resets."""
+    """Scheduling overrides (kernel, waves_per_wg, grid_wgs, depth, grid_order, tile_n, slice_m); None resets."""
     if cfg is None and not kw:
         _check(lib.rg_linear_set_launch(None), "rg_linear_set_launch")
         return

@@ -242,6 +242,48 @@ bool skinny_shape_ok(int64_t M, int64_t K) {
     return M >= 1 && K < ((int64_t)1 << 26);
 }
 
+// One slice width: S slices of mt rows of x, G row-group walkers per slice, the depth that
+// keeps the most bytes in flight per CU.  ok = false when no depth fits LDS.
+struct SkinnyGrid {
+    bool ok = false;
+    int64_t S = 0, G = 0;
+    int depth = 0, jp = 0;
+};
+
+SkinnyGrid skinny_grid(int64_t M, int64_t N, int64_t J, int64_t nw, int mt, const rg_launch_t& o) {
+    SkinnyGrid r;
+    r.S = ceil_div(M, mt);
+    const int64_t RG = ceil_div(N, 16);
+    double best_fly = -1.0;
+    for (int depth = 2; depth <= 3; ++depth) {
+        if (o.depth > 0 && depth != o.depth) continue;
+        // odd partial stride unless it costs a workgroup per CU
+        const int64_t lds_even = (int64_t)rg::skinny_lds_bytes(mt, (int)nw, depth, (int)J);
+        const int64_t lds_odd = (int64_t)rg::skinny_lds_bytes(mt, (int)nw, depth, (int)(J | 1));
+        const int jp = (lds_even > kLdsBytes || kLdsBytes / lds_odd == kLdsBytes / lds_even) ? (int)(J | 1) : (int)J;
+        const int64_t lds = jp == (int)J ? lds_even : lds_odd;
+        if (lds > kLdsBytes) continue;
+        int64_t wpc = kLdsBytes / lds;                  // workgroups per CU that LDS allows
+        const int64_t wave_cap = 8 / nw > 0 ? 8 / nw : 1;   // two waves per SIMD
+        if (wpc > wave_cap) wpc = wave_cap;
+        int64_t G = (o.grid_wgs > 0 ? o.grid_wgs : kNominalCUs * wpc) / r.S;   // walkers per slice
+        if (G < 1) G = 1;
+        if (G > RG) G = RG;
+        // bytes in flight per CU: resident workgroups x waves x depth
+        double res = (double)(G * r.S) / kNominalCUs;
+        if (res > (double)wpc) res = (double)wpc;
+        const double fly = res * (double)nw * depth;
+        if (fly > best_fly + 1e-9) {
+            best_fly = fly;
+            r.ok = true;
+            r.depth = depth;
+            r.G = G;
+            r.jp = jp;
+        }
+    }
+    return r;
+}
+
 bool skinny_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan* p) {
     if (o.tile_n != 0) return false;
     const int64_t J = ceil_div(K, rg::kChunk);
@@ -257,42 +299,27 @@ bool skinny_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan
     }
     if (spw == 3) spw = 4;
     // the widest slice whose x registers fit (narrower slices read W once more each, mostly from L2)
-    int mt = M <= 1 ? 1 : (M <= 2 ? 2 : (M <= 4 ? 4 : 8));
-    while (mt > 2 && mt * spw > 8) mt /= 2;
+    int mt = o.slice_m > 0 ? o.slice_m : (M <= 1 ? 1 : (M <= 2 ? 2 : (M <= 4 ? 4 : 8)));
+    while (mt > 1 && mt * spw > 8) mt /= 2;
     if (spw > 4 || mt * spw > 8) return false;
-    const int64_t S = ceil_div(M, mt);
-    if (S > 65536) return false;
-    const int64_t RG = ceil_div(N, 16);
-    int best_depth = 0;
-    int64_t best_g = 0;
-    double best_fly = -1.0;
-    int best_jp = 0;
-    for (int depth = 2; depth <= 3; ++depth) {
-        if (o.depth > 0 && depth != o.depth) continue;
-        // odd partial stride unless it costs a workgroup per CU
-        const int64_t lds_even = (int64_t)rg::skinny_lds_bytes(mt, (int)nw, depth, (int)J);
-        const int64_t lds_odd = (int64_t)rg::skinny_lds_bytes(mt, (int)nw, depth, (int)(J | 1));
-        const int jp = (lds_even > kLdsBytes || kLdsBytes / lds_odd == kLdsBytes / lds_even) ? (int)(J | 1) : (int)J;
-        const int64_t lds = jp == (int)J ? lds_even : lds_odd;
-        if (lds > kLdsBytes) continue;
-        int64_t wpc = kLdsBytes / lds;                  // workgroups per CU that LDS allows
-        const int64_t wave_cap = 8 / nw > 0 ? 8 / nw : 1;   // two waves per SIMD
-        if (wpc > wave_cap) wpc = wave_cap;
-        int64_t G = (o.grid_wgs > 0 ? o.grid_wgs : kNominalCUs * wpc) / S;   // walkers per slice
-        if (G < 1) G = 1;
-        if (G > RG) G = RG;
-        // bytes in flight per CU: resident workgroups x waves x depth
-        double res = (double)(G * S) / kNominalCUs;
-        if (res > (double)wpc) res = (double)wpc;
-        const double fly = res * (double)nw * depth;
-        if (fly > best_fly + 1e-9) {
-            best_fly = fly;
-            best_depth = depth;
-            best_g = G;
-            best_jp = jp;
-        }
+    if (ceil_div(M, mt) > 65536) return false;
+    SkinnyGrid g = skinny_grid(M, N, J, nw, mt, o);
+    // Where the row groups cap the walkers below the workgroups the CUs hold, halve the slice
+    // while that gives more workgroups (measured, interleaved A/B: QKV 6144 x 4096 at M = 3, 4
+    // and 8 12-19 % faster, O 4096 x 4096 at M = 2 and 8 4 %, level elsewhere; the second slice
+    // reads W from L2)
+    while (o.slice_m == 0 && o.grid_wgs == 0 && g.ok && mt > 1 && ceil_div(M, mt / 2) <= 65536) {
+        const SkinnyGrid h = skinny_grid(M, N, J, nw, mt / 2, o);
+        if (!h.ok || h.S * h.G <= g.S * g.G) break;
+        mt /= 2;
+        g = h;
     }
-    if (best_depth == 0) return false;
+    if (!g.ok) return false;
+    const int64_t RG = ceil_div(N, 16);
+    const int64_t S = g.S;
+    const int best_depth = g.depth;
+    const int64_t best_g = g.G;
+    const int best_jp = g.jp;
     if (ceil_div(RG, best_g) * 4 * spw > 0x7fffffff) return false;   // steps per wave fit int32
     p->mt = mt;
     p->rq = 4;                 // reported as 16 W rows per row group
@@ -510,7 +537,8 @@ int make_plan_f32w(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launc
 int validate_launch(const rg_launch_t& c) {
     if (c.kernel < -1 || c.kernel > 8) return RG_ERR_RANGE;
     if (c.tile_n != 0 && c.tile_n != 16 && c.tile_n != 32 && c.tile_n != 64) return RG_ERR_RANGE;
-    if (c.reserved[0] != 0 || c.reserved[1] != 0) return RG_ERR_RANGE;
+    if (c.slice_m != 0 && c.slice_m != 1 && c.slice_m != 2 && c.slice_m != 4 && c.slice_m != 8) return RG_ERR_RANGE;
+    if (c.reserved != 0) return RG_ERR_RANGE;
     if (c.waves_per_wg < 0 || c.waves_per_wg > 8) return RG_ERR_RANGE;
     if (c.grid_wgs < 0 || c.grid_wgs > 65536) return RG_ERR_RANGE;
     if (c.depth < 0 || c.depth > 3 || c.depth == 1) return RG_ERR_RANGE;

@@ -107,6 +107,31 @@ def test_gemv_schedule_defaults():
         rg.rg_linear_set_launch(None)
 
 
+def test_skinny_slice_width():
+    # where the row groups cap the walkers below the workgroups the CUs hold, the planner halves
+    # the slice of x rows while that gives more workgroups; elsewhere the widest slice that fits
+    want = {(1, 4096, 4096): 1, (2, 6144, 4096): 1, (2, 4096, 4096): 1, (3, 6144, 4096): 2,
+            (4, 6144, 4096): 2, (4, 4096, 4096): 2, (4, 28672, 4096): 4, (4, 4096, 14336): 4,
+            (4, 128256, 4096): 4, (8, 6144, 4096): 4, (16, 6144, 4096): 8, (16, 28672, 4096): 8,
+            (16, 4096, 14336): 4}
+    for shape, mt in want.items():
+        p = rg.rg_plan(*shape)
+        assert (p["kernel_name"], p["tile_m"]) == ("skinny", mt), (shape, p)
+        assert p["grid_wgs"] <= 512
+    with pytest.raises(rg.RgError):
+        rg.rg_linear_set_launch(slice_m=3)
+    try:
+        rg.rg_linear_set_launch(kernel="skinny", slice_m=8)
+        assert rg.rg_plan(4, 4096, 14336)["tile_m"] == 4      # two segment groups per wave: 4 rows fit
+        assert rg.rg_plan(4, 6144, 4096)["tile_m"] == 8       # a slice wider than M is allowed
+        rg.rg_linear_set_launch(slice_m=2)                      # not forced: applies where skinny runs
+        p = rg.rg_plan(16, 28672, 4096)
+        assert (p["kernel_name"], p["tile_m"], p["grid_wgs"]) == ("skinny", 2, 512)
+        assert rg.rg_plan(64, 28672, 4096)["kernel_name"] == "ktile"
+    finally:
+        rg.rg_linear_set_launch(None)
+
+
 def test_tiled_128_build_choice():
     # three waves per SIMD only where its rounds of 768 resident tiles are clearly fuller than
     # the two-wave build's rounds of 512; other tiles report depth 0

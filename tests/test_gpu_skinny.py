@@ -65,23 +65,27 @@ def test_ragged_shapes(M, N, K):
     _check(M, N, K, seed=M + N + K)
 
 
-@pytest.mark.parametrize("M,N,K,mt,nw", [
-    (2, 300, 4096, 2, 4),      # one segment group per wave
-    (2, 300, 9000, 2, 5),      # two per wave (J = 36)
-    (2, 100, 28672, 2, 7),     # four per wave (J = 112)
-    (4, 300, 4096, 4, 4),
-    (4, 300, 14336, 4, 7),     # two per wave
-    (8, 300, 4096, 8, 4),
-    (8, 300, 14336, 4, 7),     # x registers cap the slice at 4 rows: two slices
-    (16, 300, 28672, 2, 7),    # eight slices of 2 rows
+@pytest.mark.parametrize("M,N,K,sm,mt,nw", [
+    (2, 300, 4096, 2, 2, 4),      # one segment group per wave
+    (2, 300, 9000, 2, 2, 5),      # two per wave (J = 36)
+    (2, 100, 28672, 2, 2, 7),     # four per wave (J = 112)
+    (4, 300, 4096, 4, 4, 4),
+    (4, 300, 14336, 4, 4, 7),     # two per wave
+    (8, 300, 4096, 8, 8, 4),
+    (8, 300, 14336, 8, 4, 7),     # x registers cap the slice at 4 rows: two slices
+    (16, 300, 28672, 2, 2, 7),    # eight slices of 2 rows
+    (16, 300, 4096, 0, 1, 4),     # the planner's narrowest slices: sixteen of one row
+    (3, 6144, 4096, 0, 2, 4),     # planner: two slices of 2 rows (more workgroups)
+    (8, 4096, 4096, 0, 4, 4),     # planner: two slices of 4 rows
 ])
-def test_every_build(M, N, K, mt, nw):
-    _check(M, N, K, seed=N + K, expect={"tile_m": mt, "waves_per_wg": nw})
+def test_every_build(M, N, K, sm, mt, nw):
+    _check(M, N, K, seed=N + K, cfg=dict(slice_m=sm) if sm else None, expect={"tile_m": mt, "waves_per_wg": nw})
 
 
 @pytest.mark.parametrize("cfg", [dict(depth=2), dict(depth=3), dict(depth=2, grid_order=1), dict(grid_wgs=1),
                                  dict(grid_wgs=3, depth=3), dict(grid_wgs=1000, grid_order=1),
-                                 dict(waves_per_wg=8), dict(waves_per_wg=2, depth=2), dict(waves_per_wg=1, grid_wgs=7)])
+                                 dict(waves_per_wg=8), dict(waves_per_wg=2, depth=2), dict(waves_per_wg=1, grid_wgs=7),
+                                 dict(slice_m=1), dict(slice_m=2, depth=3), dict(slice_m=8, grid_wgs=5)])
 @pytest.mark.parametrize("M,N,K", [(4, 1030, 4096), (3, 515, 2056), (16, 259, 4352)])
 def test_launch_overrides_do_not_change_bits(M, N, K, cfg):
     import paper_2609_25624_amd as rg
