@@ -443,7 +443,15 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     const bool skinny_ok = fast_ok && skinny_shape_ok(M, K);
     // M == 1 too: the one-row skinny build measured 2 % faster than the GEMV on the
     // 28672 x 4096, 4096 x 14336 and 128256 x 4096 layers and level on the two narrow ones
-    if (skinny_ok && M <= kSkinnyMaxM) want = RG_KERNEL_SKINNY;
+    // 16 < M <= 64: skinny where ktile's tiles are narrow (fewer than 448 of 64 W rows: every
+    // ktile workgroup re-reads all of x) and x of two segment groups fits (K <= 16384).
+    // Measured, interleaved A/B: QKV 6144 x 4096 at M = 32 / 48 / 64 40.6 / 83.3 / 73.8 against
+    // 71.7 / 86.7 / 89.8 us, O 4096 x 4096 at M = 24 / 32 / 64 33.2 / 29.6 / 51.5 against
+    // 36.3 / 39.4 / 65.5, down 4096 x 14336 at M = 32 113 against 133 (level at M = 64);
+    // ktile stays faster on gate+up 28672 x 4096 and the 70B down 8192 x 28672
+    const bool skinny_mid = skinny_ok && M > kSkinnyMaxM && M <= kDecodeMaxM && ceil_div(N, 64) < 448 &&
+                            ceil_div(J, 4) <= 16;
+    if (skinny_ok && (M <= kSkinnyMaxM || skinny_mid)) want = RG_KERNEL_SKINNY;
     else if (gemv_ok && ceil_div(K, rg::kChunk) == 16) want = RG_KERNEL_GEMV;
     else if (ktile_ok && ktile_pref) want = RG_KERNEL_KTILE;
     else if (decode_ok && M <= kDecodeMaxM) want = (M == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;

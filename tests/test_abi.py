@@ -132,6 +132,15 @@ def test_skinny_slice_width():
         rg.rg_linear_set_launch(None)
 
 
+def test_mid_batch_kernel_choice():
+    # 16 < M <= 64: skinny on layers with fewer than 448 tiles of 64 W rows and K <= 16384,
+    # ktile on the wide ones and where x of a wave's segment groups would not fit
+    for shape, name in (((32, 6144, 4096), "skinny"), ((64, 4096, 4096), "skinny"), ((64, 4096, 14336), "skinny"),
+                        ((17, 300, 1000), "skinny"), ((32, 28672, 4096), "ktile"), ((64, 128256, 4096), "ktile"),
+                        ((64, 8192, 28672), "ktile"), ((17, 4096, 16640), "ktile"), ((65, 4096, 4096), "tiled")):
+        assert rg.rg_plan(*shape)["kernel_name"] == name, shape
+
+
 def test_tiled_128_build_choice():
     # three waves per SIMD only where its rounds of 768 resident tiles are clearly fuller than
     # the two-wave build's rounds of 512; other tiles report depth 0

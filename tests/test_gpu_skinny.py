@@ -1,4 +1,4 @@
-"""The skinny kernel (M <= 16: 16 W rows x 4 segments per wave, x shared by the 16 lanes of a
+"""The skinny kernel (M <= 16, and to M = 64 on narrow layers: 16 W rows x 4 segments per wave, x shared by the 16 lanes of a
 DPP row) against the oracle, bit for bit.
 
 Shapes cover the batched-decode layers of an 8B Llama-3-class model (Supplement A, decode
@@ -63,6 +63,14 @@ def test_llama_decode_layers_full_output(M, N, K):
                                  (77, 9000), (31, 14336), (19, 28672)])
 def test_ragged_shapes(M, N, K):
     _check(M, N, K, seed=M + N + K)
+
+
+@pytest.mark.parametrize("M", [17, 24, 33, 64])
+@pytest.mark.parametrize("N,K", [(4096, 4096), (259, 14336), (1030, 2056)])
+def test_mid_batch_narrow_layers(M, N, K):
+    """16 < M <= 64 on layers with few 64-row tiles: the planner's skinny kernel, several
+    slices of x with a short last one."""
+    _check(M, N, K, seed=M * 3 + N)
 
 
 @pytest.mark.parametrize("M,N,K,sm,mt,nw", [
