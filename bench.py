@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--profile-shape", metavar="M,N,K",
                     help="short run for hardware counters: 20 launches of rg_linear at this shape (seeded inputs, "
                          "three rotated weight copies), then exit")
+    ap.add_argument("--profile-kernel", metavar="NAME",
+                    help="with --profile-shape: force this kernel (a name of rg_plan's kernel_name)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("COUNTER_CSV", "M,N,K"),
                     help="summarise a rocprofv3 --pmc CSV of a --profile-shape run: per-launch counter averages and "
                          "derived issue rates (no GPU needed) and exit")
@@ -199,8 +201,9 @@ def run_floors():
         torch.cuda.empty_cache()
 
 
-def profile_shape(M, N, K):
-    """Dispatches for rocprofv3 counter runs of one shape: 20 launches of rg_linear."""
+def profile_shape(M, N, K, kernel=None):
+    """Dispatches for rocprofv3 counter runs of one shape: 20 launches of rg_linear (the planner's
+    kernel, or `kernel` forced)."""
     import numpy as np
     import torch
 
@@ -212,6 +215,8 @@ def profile_shape(M, N, K):
     ws = [torch.from_numpy(w.view(np.int16)).to(dev)]
     ws += [ws[0].clone() for _ in range(2)]
     y = torch.empty((M, N), dtype=torch.float32, device=dev)
+    if kernel:
+        rg.rg_linear_set_launch(kernel=kernel)
     torch.cuda.synchronize()
     for i in range(20):
         rg.rg_linear(xd, ws[i % 3], y)
@@ -682,7 +687,7 @@ def main():
         profile_kernels()
         return
     if args.profile_shape:
-        profile_shape(*[int(v) for v in args.profile_shape.split(",")])
+        profile_shape(*[int(v) for v in args.profile_shape.split(",")], kernel=args.profile_kernel)
         return
     if args.configs:
         run_configs()

@@ -82,9 +82,13 @@ typedef enum {
                                 (FP32 weights by default; BF16 weights when forced) */
     RG_KERNEL_KTILE = 6,     /* 16 < M <= 64 (any M when forced): 4 x 4 register tiles, K segments
                                 shared out over thread groups */
-    RG_KERNEL_SKINNY = 7     /* M <= 16: waves of 16 W rows x 4 segments, x of a segment shared
-                                by 16 lanes through DPP row broadcasts, slices of 1, 2, 4 or 8
-                                rows of x */
+    RG_KERNEL_SKINNY = 7,    /* M <= 16, and narrow layers to M = 64: waves of 16 W rows x 4
+                                segments, x of a segment shared by 16 lanes through DPP row
+                                broadcasts, slices of 1, 2, 4 or 8 rows of x */
+    RG_KERNEL_WTILE = 8      /* 32 < M <= 64 on wide layers: 64 x 64 output tiles, each wave the
+                                whole tile for one segment at a time (8 x 8 chains per lane),
+                                its own LDS slabs, the partials added wave by wave in segment
+                                order */
 } rg_kernel_id;
 
 /* Scheduling overrides for the determinism tests.  0 in a field = planner
@@ -95,7 +99,8 @@ typedef enum {
  *                    call returns RG_ERR_RANGE)
  *   waves_per_wg  : 1..8  waves (64 threads each) per workgroup (gemv: 1..4, and 1, 2
  *                   or 4 when K > 4096; ktile: 4, or 8 with tile_n 16; skinny: any count
- *                   whose ceil(J / 4 / waves) segment groups per wave fit its registers)
+ *                   whose ceil(J / 4 / waves) segment groups per wave fit its registers;
+ *                   wtile: 4 or 8)
  *   grid_wgs      : 1..65536 workgroups (work is spread over them evenly)
  *   depth         : 2..3  decode pipeline depth in 128-byte-per-row slabs (unused by gemv);
  *                   tiled kernel with 128 x 128 tiles: the build for 2 or 3 waves per SIMD;

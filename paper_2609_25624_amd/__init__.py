@@ -12,7 +12,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librg.so")
 
 RG_OK, RG_ERR_INVAL, RG_ERR_ALIGN, RG_ERR_ARCH, RG_ERR_HIP, RG_ERR_RANGE, RG_ERR_ALIAS = range(7)
-KERNELS = {0: "generic", 1: "decode", 2: "tiled", 3: "decode_xs", 4: "gemv", 5: "stream", 6: "ktile", 7: "skinny"}
+KERNELS = {0: "generic", 1: "decode", 2: "tiled", 3: "decode_xs", 4: "gemv", 5: "stream", 6: "ktile", 7: "skinny", 8: "wtile"}
 CHUNK = 256
 
 

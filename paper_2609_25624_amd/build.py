@@ -17,7 +17,7 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-fast-math",
           "-fno-gpu-flush-denormals-to-zero", "-Wall", "-Wno-unused-result"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-SOURCES = ["rg_kernels.hip", "rg_attn.hip", "rg_api.cpp"]
+SOURCES = ["rg_kernels.hip", "rg_wtile.hip", "rg_attn.hip", "rg_api.cpp"]
 # Negative controls (kernels that break the design rules on purpose, for the tests): a library of their own.
 NEGCTL_LIB = os.path.join(HERE, "librg_negctl.so")
 NEGCTL_SOURCES = ["rg_negctl.hip"]

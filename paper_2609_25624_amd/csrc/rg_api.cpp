@@ -16,6 +16,7 @@
 #include "../../include/rg.h"
 #include "../../include/rg_attn.h"
 #include "rg_kernels.h"
+#include "rg_wtile.h"
 
 namespace {
 
@@ -227,6 +228,22 @@ bool ktile_schedule(int64_t M, int64_t N, int64_t K, const rg_launch_t& o, Plan*
     p->nw = nw;
     p->cn = cn;
     p->depth = cn == 8 ? 3 : 2;
+    return true;
+}
+
+// Wave-tile kernel: 64 x 64 tiles, one per workgroup of four waves (eight when forced: more
+// segments in flight per tile, one workgroup per CU); the grid order applies.
+bool wtile_schedule(int64_t M, int64_t N, const rg_launch_t& o, Plan* p) {
+    if ((o.waves_per_wg != 0 && o.waves_per_wg != 4 && o.waves_per_wg != 8) || o.grid_wgs != 0 || o.depth != 0 ||
+        (o.tile_n != 0 && o.tile_n != 64) || o.slice_m != 0)
+        return false;
+    const int64_t tiles = ceil_div(M, rg::kWtileRows) * ceil_div(N, rg::kWtileRows);
+    if (tiles > 0x7fffffff) return false;
+    p->tile_m = rg::kWtileRows;
+    p->tile_n = rg::kWtileRows;
+    p->grid = (int)tiles;
+    p->nw = o.waves_per_wg > 0 ? o.waves_per_wg : 4;
+    p->depth = 0;
     return true;
 }
 
@@ -451,7 +468,14 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     // ktile stays faster on gate+up 28672 x 4096 and the 70B down 8192 x 28672
     const bool skinny_mid = skinny_ok && M > kSkinnyMaxM && M <= kDecodeMaxM && ceil_div(N, 64) < 448 &&
                             ceil_div(J, 4) <= 16;
+    // 32 < M <= 64 on wide layers with at most 1024 tiles of 64 W rows: the wave-tile kernel
+    // (interleaved A/B against ktile: gate+up 28672 x 4096 at M = 40 / 64 219 / 225 against
+    // 250 / 252 us, 70B gate+up 57344 x 8192 at M = 64 858 against 944; level on the
+    // 128256-row LM head, whose 2004 tiles already fill the CUs under ktile)
+    const bool wtile_pref = fast_ok && M > 32 && M <= kDecodeMaxM && ceil_div(N, 64) >= 448 &&
+                            ceil_div(N, 64) <= 1024;
     if (skinny_ok && (M <= kSkinnyMaxM || skinny_mid)) want = RG_KERNEL_SKINNY;
+    else if (wtile_pref) want = RG_KERNEL_WTILE;
     else if (gemv_ok && ceil_div(K, rg::kChunk) == 16) want = RG_KERNEL_GEMV;
     else if (ktile_ok && ktile_pref) want = RG_KERNEL_KTILE;
     else if (decode_ok && M <= kDecodeMaxM) want = (M == 1) ? RG_KERNEL_DECODE_XS : RG_KERNEL_DECODE;
@@ -466,6 +490,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         if (want == RG_KERNEL_KTILE && !fast_ok) return RG_ERR_RANGE;   // any M when forced
         if (want == RG_KERNEL_STREAM && !(fast_ok && M <= 4)) return RG_ERR_RANGE;
         if (want == RG_KERNEL_SKINNY && !skinny_ok) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_WTILE && !fast_ok) return RG_ERR_RANGE;
     }
     p->mslices = 1;
     p->kernel = want;
@@ -481,6 +506,11 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
         else
             want = p->kernel = (ktile_ok && ktile_pref) ? RG_KERNEL_KTILE
                              : (decode_ok ? RG_KERNEL_DECODE : (tiled_ok ? RG_KERNEL_TILED : RG_KERNEL_GENERIC));
+    }
+    if (want == RG_KERNEL_WTILE) {
+        if (wtile_schedule(M, N, o, p)) return RG_OK;
+        if (forced) return RG_ERR_RANGE;
+        want = p->kernel = RG_KERNEL_KTILE;   // overrides the wave-tile kernel does not take
     }
     if (want == RG_KERNEL_KTILE) {
         if (ktile_schedule(M, N, K, o, p)) return RG_OK;
@@ -528,7 +558,9 @@ int make_plan_f32w(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launc
     const bool forced = o.kernel > 0;
     if (forced) {
         want = o.kernel - 1;
-        if (want == RG_KERNEL_DECODE || want == RG_KERNEL_DECODE_XS || want == RG_KERNEL_GEMV) return RG_ERR_RANGE;
+        if (want == RG_KERNEL_DECODE || want == RG_KERNEL_DECODE_XS || want == RG_KERNEL_GEMV ||
+            want == RG_KERNEL_SKINNY)
+            return RG_ERR_RANGE;
         if (want != RG_KERNEL_GENERIC && !fast_ok) return RG_ERR_RANGE;
         if (want == RG_KERNEL_STREAM && M > 4) return RG_ERR_RANGE;
     }
@@ -537,13 +569,14 @@ int make_plan_f32w(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launc
     p->mslices = 1;
     if (want == RG_KERNEL_STREAM) return stream_schedule(M, N, o, p) ? RG_OK : RG_ERR_RANGE;
     if (want == RG_KERNEL_KTILE) return ktile_schedule(M, N, K, o, p) ? RG_OK : RG_ERR_RANGE;
+    if (want == RG_KERNEL_WTILE) return wtile_schedule(M, N, o, p) ? RG_OK : RG_ERR_RANGE;
     if (want == RG_KERNEL_TILED) return tiled_schedule(M, N, o, p);
     generic_schedule(M, N, o, p);
     return RG_OK;
 }
 
 int validate_launch(const rg_launch_t& c) {
-    if (c.kernel < -1 || c.kernel > 8) return RG_ERR_RANGE;
+    if (c.kernel < -1 || c.kernel > 9) return RG_ERR_RANGE;
     if (c.tile_n != 0 && c.tile_n != 16 && c.tile_n != 32 && c.tile_n != 64) return RG_ERR_RANGE;
     if (c.slice_m != 0 && c.slice_m != 1 && c.slice_m != 2 && c.slice_m != 4 && c.slice_m != 8) return RG_ERR_RANGE;
     if (c.reserved != 0) return RG_ERR_RANGE;
@@ -728,6 +761,8 @@ int linear_impl(const float* x, const uint16_t* w, const float* bias, float* y, 
         e = launch_stream(x, w, bias, y, M, N, K, p, false, st);
     } else if (p.kernel == RG_KERNEL_KTILE) {
         e = rg::launch_ktile(x, w, bias, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.cn, p.reverse, st);
+    } else if (p.kernel == RG_KERNEL_WTILE) {
+        e = rg::launch_wtile(x, w, bias, y, M, N, K, p.nw, p.reverse, st);
     } else if (p.kernel == RG_KERNEL_TILED) {
         e = rg::launch_tiled(x, w, bias, y, M, N, K, p.tile_m, p.tile_n, p.depth, p.reverse, st);
     } else {
@@ -756,6 +791,8 @@ int linear_f32w_impl(const float* x, const float* w, float* y, int64_t M, int64_
         e = launch_stream(x, w, nullptr, y, M, N, K, p, true, st);
     } else if (p.kernel == RG_KERNEL_KTILE) {
         e = rg::launch_ktile(x, w, nullptr, y, M, N, K, p.tile_m, p.tile_n, 64 * p.nw, p.cn, p.reverse, st);
+    } else if (p.kernel == RG_KERNEL_WTILE) {
+        e = rg::launch_wtile(x, w, nullptr, y, M, N, K, p.nw, p.reverse, st);
     } else if (p.kernel == RG_KERNEL_TILED) {
         e = rg::launch_tiled(x, w, nullptr, y, M, N, K, p.tile_m, p.tile_n, p.depth, p.reverse, st);
     } else {

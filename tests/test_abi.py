@@ -133,12 +133,19 @@ def test_skinny_slice_width():
 
 
 def test_mid_batch_kernel_choice():
-    # 16 < M <= 64: skinny on layers with fewer than 448 tiles of 64 W rows and K <= 16384,
-    # ktile on the wide ones and where x of a wave's segment groups would not fit
+    # 16 < M <= 64: skinny on layers with fewer than 448 tiles of 64 W rows and K <= 16384, the
+    # wave-tile kernel above M = 32 with 448 to 1024 such tiles, ktile elsewhere
     for shape, name in (((32, 6144, 4096), "skinny"), ((64, 4096, 4096), "skinny"), ((64, 4096, 14336), "skinny"),
                         ((17, 300, 1000), "skinny"), ((32, 28672, 4096), "ktile"), ((64, 128256, 4096), "ktile"),
+                        ((33, 28672, 4096), "wtile"), ((64, 28672, 4096), "wtile"), ((64, 57344, 8192), "wtile"),
                         ((64, 8192, 28672), "ktile"), ((17, 4096, 16640), "ktile"), ((65, 4096, 4096), "tiled")):
         assert rg.rg_plan(*shape)["kernel_name"] == name, shape
+    rg.rg_linear_set_launch(tile_n=32)          # not forced, not a wave-tile setting: ktile takes it
+    try:
+        p = rg.rg_plan(64, 28672, 4096)
+        assert (p["kernel_name"], p["tile_n"]) == ("ktile", 32)
+    finally:
+        rg.rg_linear_set_launch(None)
 
 
 def test_tiled_128_build_choice():
@@ -160,7 +167,7 @@ def test_tiled_128_build_choice():
 
 
 def test_set_launch_range_checks():
-    for bad in (dict(waves_per_wg=9), dict(grid_wgs=-1), dict(depth=4), dict(depth=1), dict(grid_order=2), dict(kernel=9), dict(tile_n=48)):
+    for bad in (dict(waves_per_wg=9), dict(grid_wgs=-1), dict(depth=4), dict(depth=1), dict(grid_order=2), dict(kernel=10), dict(tile_n=48)):
         with pytest.raises(rg.RgError) as e:
             rg.rg_linear_set_launch(**bad)
         assert e.value.code == rg.RG_ERR_RANGE
@@ -201,18 +208,20 @@ def test_other_entry_points_reject_bad_arguments():
     assert L.rg_device_cu_count(None) == rg.RG_ERR_INVAL
 
 
-def test_no_atomics_or_matrix_core_builtins_in_kernels():
-    src = open(os.path.join(ROOT, "paper_2609_25624_amd", "csrc", "rg_kernels.hip")).read()
+@pytest.mark.parametrize("fname", ["rg_kernels.hip", "rg_wtile.hip"])
+def test_no_atomics_or_matrix_core_builtins_in_kernels(fname):
+    src = open(os.path.join(ROOT, "paper_2609_25624_amd", "csrc", fname)).read()
     code = re.sub(r"//.*", "", src)
     for bad in ("atomicAdd", "__hip_atomic", "mfma", "__builtin_amdgcn_fdot", "__builtin_amdgcn_sdot",
                 "unsafe-fp", "fast-math"):
         assert bad not in code, bad
 
 
-def test_device_code_uses_only_ieee_fma_for_accumulation():
+@pytest.mark.parametrize("fname", ["rg_kernels.hip", "rg_wtile.hip"])
+def test_device_code_uses_only_ieee_fma_for_accumulation(fname):
     # Inspect the gfx950 assembly of our own kernels: no matrix-core, dot-product,
     # packed-FP32, mixed-precision or non-fused multiply-add instructions.
-    asm = _device_asm("rg_kernels.hip")
+    asm = _device_asm(fname)
     insts = re.findall(r"^\s+(v_[a-z0-9_]+)", asm, flags=re.M)
     assert insts
     for i in set(insts):
@@ -365,7 +374,7 @@ def test_inline_assembly_writes_no_register_asynchronously():
     and faulted).  The only memory instruction the library's inline assembly may issue is the
     global->LDS DMA (no register destination); every other asm instruction is synchronous."""
     allowed = {"s_nop", "s_mov_b32", "s_add_u32", "global_load_lds_dwordx4", "s_waitcnt", "v_fmac_f32_dpp"}
-    for f in ("rg_kernels.hip", "rg_attn.hip"):
+    for f in ("rg_kernels.hip", "rg_wtile.hip", "rg_attn.hip"):
         asm = _device_asm(f)
         blocks = re.findall(r";;#ASMSTART\n(.*?);;#ASMEND", asm, flags=re.S)
         ops = {ln.split()[0] for blk in blocks for ln in blk.splitlines() if ln.strip() and not ln.strip().startswith(";")}

@@ -92,6 +92,7 @@ def _kernel_cases():
         ("stream", 1, 33, 264), ("stream", 4, 130, 4352),
         ("tiled", 100, 1000, 1000), ("tiled", 129, 257, 264),
         ("skinny", 2, 33, 264), ("skinny", 4, 1030, 4104), ("skinny", 9, 77, 1000), ("skinny", 16, 130, 4096),
+        ("wtile", 64, 130, 1000), ("wtile", 40, 77, 264), ("wtile", 65, 70, 8),
     ]
 
 
