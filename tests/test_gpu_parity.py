@@ -424,6 +424,10 @@ def _launch_settings():
         dict(kernel="skinny", depth=3, grid_order=1),
         dict(kernel="skinny", depth=2, grid_wgs=5),
         dict(kernel="skinny", waves_per_wg=8, grid_wgs=1000, grid_order=1),
+        dict(kernel="skinny", slice_m=1),
+        dict(kernel="wtile"),
+        dict(kernel="wtile", grid_order=1),
+        dict(kernel="wtile", waves_per_wg=8),
     ]
 
 
@@ -460,30 +464,34 @@ def test_cu_masks_do_not_change_bits():
         "alternate": [0x55555555] * nwords,
         "first64": [0xFFFFFFFF if i < 2 else 0 for i in range(nwords)],
     }
-    M, N, K = 1, 6144, 4096
-    x, w = gu.layer(M, N, K, seed=31)
-    xd, wd = gu.to_dev(x, w)
-    want = gu.oracle_full(x, w)
+    # the M = 1 step's QKV layer, two slices of the skinny kernel, and the wave-tile kernel
+    cases = [((1, 6144, 4096), None), ((16, 2048, 4096), None), ((40, 1030, 4096), dict(kernel="wtile"))]
     done = 0
-    for name, mask in masks.items():
-        try:
-            s = rg.rg_stream_create_cu_mask(mask)
-        except rg.RgError as e:
-            gu.log(f"  cu mask {name}: the runtime refused it ({e})")
-            continue
-        try:
-            ext = torch.cuda.ExternalStream(s)
-            y = torch.empty((M, N), dtype=torch.float32, device=gu.dev())
-            torch.cuda.synchronize()
-            gu.run(xd, wd, stream=ext, out=y)
-            ext.synchronize()
-            gu.log(f"  cu mask {name}: done")
-            gu.assert_bitwise(y.cpu().numpy(), want, f"cu mask {name}")
-            done += 1
-        finally:
-            torch.cuda.synchronize()
-            rg.rg_stream_destroy(s)
-    assert done >= 3, "fewer than three CU masks could be exercised"
+    for (M, N, K), cfg in cases:
+        rg.rg_linear_set_launch(**cfg) if cfg else rg.rg_linear_set_launch(None)
+        x, w = gu.layer(M, N, K, seed=31)
+        xd, wd = gu.to_dev(x, w)
+        want = gu.oracle_full(x, w)
+        for name, mask in masks.items():
+            try:
+                s = rg.rg_stream_create_cu_mask(mask)
+            except rg.RgError as e:
+                gu.log(f"  cu mask {name}: the runtime refused it ({e})")
+                continue
+            try:
+                ext = torch.cuda.ExternalStream(s)
+                y = torch.empty((M, N), dtype=torch.float32, device=gu.dev())
+                torch.cuda.synchronize()
+                gu.run(xd, wd, stream=ext, out=y)
+                ext.synchronize()
+                gu.log(f"  ({M},{N},{K}) {rg.rg_plan(M, N, K)['kernel_name']} cu mask {name}: done")
+                gu.assert_bitwise(y.cpu().numpy(), want, f"({M},{N},{K}) cu mask {name}")
+                done += 1
+            finally:
+                torch.cuda.synchronize()
+                rg.rg_stream_destroy(s)
+    rg.rg_linear_set_launch(None)
+    assert done >= 9, "fewer than three CU masks per case could be exercised"
 
 
 def test_fifty_repeats_one_distinct_output():
