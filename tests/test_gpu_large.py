@@ -28,6 +28,7 @@ def _reset_launch():
                                                  (1, 1048579, 2304, "decode_xs", True), (1, 524309, 4096, "gemv", True),
                                                  (3, 1048579, 2304, "skinny", False), (16, 1048579, 2304, "skinny", False),
                                                  (3, 1048579, 2304, "decode", True), (16, 1048579, 2304, "ktile", True),
+                                                 (40, 1048579, 2304, "wtile", True), (40, 1048579, 2304, "skinny", True),
                                                  (70, 1048579, 2304, "tiled", False)])
 def test_weights_beyond_4_gib(M, N, K, kernel, forced):
     import torch
