@@ -2014,13 +2014,11 @@ __global__ void __launch_bounds__(256) cast_kernel(const uint16_t* __restrict__ 
 // exact, so the result does not depend on the reduction tree.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ bool better(float v, int64_t i, float bv, int64_t bi) {
-    if (v != v) return false;
-    if (bi < 0 || bv != bv) return true;
-    return v > bv || (v == bv && i < bi);
+    return (v == v) & ((bi < 0) | (bv != bv) | (v > bv) | ((v == bv) & (i < bi)));
 }
 
 constexpr int kArgmaxThreads = 1024;
-constexpr int kArgmaxBatch = 16;     // independent loads in flight per thread
+constexpr int kArgmaxBatch = 16;     // independent loads in flight per thread (4 or 16 bytes each)
 
 __global__ void __launch_bounds__(kArgmaxThreads) argmax_kernel(const float* __restrict__ y, int64_t* __restrict__ out,
                                                                 int64_t N) {
@@ -2032,6 +2030,32 @@ __global__ void __launch_bounds__(kArgmaxThreads) argmax_kernel(const float* __r
     int64_t bi = -1;
     constexpr int64_t step = (int64_t)kArgmaxThreads * kArgmaxBatch;
     int64_t n0 = threadIdx.x;
+    if (N % 4 == 0 && ((uintptr_t)row & 15) == 0) {
+        // 16-byte loads: a row of the 128256-entry LM head is two rounds of 16 loads per thread
+        const float4* row4 = reinterpret_cast<const float4*>(row);
+        const int64_t N4 = N / 4;
+        for (int64_t q0 = threadIdx.x; q0 < N4; q0 += step) {
+            float4 v[kArgmaxBatch];
+#pragma unroll
+            for (int u = 0; u < kArgmaxBatch; ++u) {
+                const int64_t q = q0 + (int64_t)u * kArgmaxThreads;
+                v[u] = q < N4 ? row4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int u = 0; u < kArgmaxBatch; ++u) {
+                const int64_t q = q0 + (int64_t)u * kArgmaxThreads;
+                if (q >= N4) continue;
+                const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    const bool take = better(e[h], 4 * q + h, bv, bi);   // selects, not branches
+                    bv = take ? e[h] : bv;
+                    bi = take ? 4 * q + h : bi;
+                }
+            }
+        }
+        n0 = N;   // nothing left for the scalar loops
+    }
     for (; n0 + (kArgmaxBatch - 1) * kArgmaxThreads < N; n0 += step) {
         float v[kArgmaxBatch];
 #pragma unroll

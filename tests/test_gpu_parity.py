@@ -583,3 +583,30 @@ def test_argmax_kernel_ties_and_nan():
     rg.rg_argmax_rows(yb, idx)
     torch.cuda.synchronize()
     assert idx.cpu().tolist() == [oracle.argmax(big[i]) for i in range(3)] == [99999, 17, 0]
+
+
+@pytest.mark.parametrize("N,offset", [(128256, 0), (100003, 0), (128256, 1), (7, 0), (65540, 0)])
+def test_argmax_kernel_paths(N, offset):
+    # 16-byte loads where the row length is a multiple of 4 and the rows are 16-byte aligned,
+    # 4-byte loads otherwise (offset 1 shifts the rows off alignment); ties and NaNs in every
+    # position of a 16-byte vector, and the winner in the last element
+    import torch
+    import oracle
+    import paper_2609_25624_amd as rg
+    rng = np.random.default_rng(N + offset)
+    M = 6
+    y = rng.standard_normal((M, N)).astype(np.float32)
+    y[0, :] = 1.0                                   # all tied: index 0
+    y[1, [N - 1, N // 2]] = 9.0                     # tie: the lower index
+    y[2, ::3] = np.nan                              # NaNs never win
+    y[3, N - 1] = 50.0                              # the winner is the last element
+    y[4, :] = np.nan
+    y[4, min(N - 1, 5)] = -3.0                      # one number among NaNs
+    flat = np.zeros(M * N + offset, dtype=np.float32)
+    flat[offset:] = y.ravel()
+    base = torch.from_numpy(flat).to(gu.dev())
+    yd = base[offset:].view(M, N)
+    idx = torch.empty(M, dtype=torch.int64, device=gu.dev())
+    rg.rg_argmax_rows(yd, idx)
+    torch.cuda.synchronize()
+    assert idx.cpu().tolist() == [oracle.argmax(y[i]) for i in range(M)]
