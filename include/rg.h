@@ -135,7 +135,7 @@ typedef struct {
     int32_t depth;         /* decode: pipeline depth; tiled 128 x 128: waves per SIMD (2 or 3);
                               ktile: 2 = 4 x 4, 3 = 4 x 8 outputs per thread */
     int32_t rows_per_round;/* decode: W rows per workgroup round; skinny: 16 */
-    int32_t tile_m, tile_n;/* tiled: output tile; skinny: rows of x per slice, 16 W rows */
+    int32_t tile_m, tile_n;/* tiled, ktile, wtile: output tile; skinny: rows of x per slice, 16 W rows */
 } rg_plan_t;
 
 /*
@@ -173,9 +173,9 @@ int rg_linear_bias(const float* x, const uint16_t* w_bf16, const float* bias, fl
  *   x      device pointer, float32 [M][K], 4-byte aligned
  *   w_f32  device pointer, float32 [N][K], 4-byte aligned
  *   y      device pointer, float32 [M][N], 4-byte aligned, must not overlap x or W
- * Kernels: RG_KERNEL_STREAM for M <= 4, then ktile (M <= 64) and tiled,
- * all needing 16-byte aligned x and W and K % 4 == 0; other shapes take the
- * generic kernel.  Errors, streams and ownership as rg_linear; the same
+ * Kernels: RG_KERNEL_STREAM for M <= 4, then ktile (M <= 64) and tiled
+ * (wtile when forced), all needing 16-byte aligned x and W and K % 4 == 0;
+ * other shapes take the generic kernel.  Errors, streams and ownership as rg_linear; the same
  * rg_linear_set_launch overrides apply (decode, decode_xs and gemv cannot be
  * forced here: RG_ERR_RANGE).
  */
@@ -183,11 +183,16 @@ int rg_linear_f32w(const float* x, const float* w_f32, float* y, int64_t M, int6
 
 /* Set (cfg != NULL) or reset (cfg == NULL) the scheduling overrides used by
  * later rg_linear, rg_linear_bias and rg_linear_f32w calls.  RG_ERR_RANGE if a
- * field is out of range. */
+ * field is out of range.  They exist to show rules R2-R3 hold (Design, R2-R3;
+ * Supplement C, the schedule ablations): moving work between workgroups,
+ * waves and compute units changes no bit. */
 int rg_linear_set_launch(const rg_launch_t* cfg);
 
 /* Fill *out with the plan for (M, N, K) under the current overrides.  A pure
- * function of its arguments and the overrides; queries no device.  CPU safe. */
+ * function of its arguments and the overrides; queries no device.  CPU safe.
+ * Rule R2 (Design): the configuration, and with it every bit of the result,
+ * is a function of the shape alone; the segment length C and count J that fix
+ * the order depend on K alone (Design, R3). */
 int rg_plan(int64_t M, int64_t N, int64_t K, rg_plan_t* out);
 
 /* The same for rg_linear_f32w (FP32 weights). */
