@@ -697,7 +697,20 @@ __global__ void __launch_bounds__(256) attn_fold_kernel(AttnArgs a) {
         const float* np = a.npart + bh * a.J * D + d;
         float S = 0.0f, N = 0.0f;
         int jj = 0;
-        for (; jj + 8 <= Jb; jj += 8) {            // loads issued in groups, additions in order
+        for (; jj + 32 <= Jb; jj += 32) {          // loads issued in groups, additions in order
+            float sv[32], nv[32];
+#pragma unroll
+            for (int i = 0; i < 32; ++i) {
+                sv[i] = sp[jj + i];
+                nv[i] = np[(int64_t)(jj + i) * D];
+            }
+#pragma unroll
+            for (int i = 0; i < 32; ++i) {
+                S = (jj + i == 0) ? sv[i] : S + sv[i];
+                N = (jj + i == 0) ? nv[i] : N + nv[i];
+            }
+        }
+        for (; jj + 8 <= Jb; jj += 8) {
             float sv[8], nv[8];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
