@@ -459,7 +459,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     const bool ktile_pref = M > 8 || (M > 4 && ceil_div(N, 16) >= 384);
     const bool skinny_ok = fast_ok && skinny_shape_ok(M, K);
     // M == 1 too: the one-row skinny build measured 2 % faster than the GEMV on the
-    // 28672 x 4096, 4096 x 14336 and 128256 x 4096 layers and level on the two narrow ones
+    // 28672 x 4096, 4096 x 14336 and 128256 x 4096 layers
     // 16 < M <= 64: skinny where ktile's tiles are narrow (fewer than 448 of 64 W rows: every
     // ktile workgroup re-reads all of x) and x of two segment groups fits (K <= 16384).
     // Measured, interleaved A/B: QKV 6144 x 4096 at M = 32 / 48 / 64 40.6 / 83.3 / 73.8 against
@@ -474,7 +474,14 @@ int make_plan(int64_t M, int64_t N, int64_t K, bool fast_ok, const rg_launch_t& 
     // 128256-row LM head, whose 2004 tiles already fill the CUs under ktile)
     const bool wtile_pref = fast_ok && M > 32 && M <= kDecodeMaxM && ceil_div(N, 64) >= 448 &&
                             ceil_div(N, 64) <= 1024;
-    if (skinny_ok && (M <= kSkinnyMaxM || skinny_mid)) want = RG_KERNEL_SKINNY;
+    // M == 1, one 16-segment step per row (K = 4096), N <= 4096: the GEMV's 32 KB bursts put a
+    // wave's whole share of W in flight at once, which these short launches need (timed the way
+    // the benchmark times, events on the launch stream: 4096 x 4096 8.1 against the skinny
+    // kernel's 9.2 us, 2048 x 4096 7.2 against 7.8; skinny from 6144 rows on: 11.2 / 13.1 / 36.3
+    // against 11.3 / 13.6 / 37.0 at 6144 / 8192 / 28672)
+    const bool gemv_short = gemv_ok && ceil_div(K, rg::kChunk) == 16 && N <= 4096;
+    if (gemv_short) want = RG_KERNEL_GEMV;
+    else if (skinny_ok && (M <= kSkinnyMaxM || skinny_mid)) want = RG_KERNEL_SKINNY;
     else if (wtile_pref) want = RG_KERNEL_WTILE;
     else if (gemv_ok && ceil_div(K, rg::kChunk) == 16) want = RG_KERNEL_GEMV;
     else if (ktile_ok && ktile_pref) want = RG_KERNEL_KTILE;

@@ -110,7 +110,7 @@ def test_gemv_schedule_defaults():
 def test_skinny_slice_width():
     # where the row groups cap the walkers below the workgroups the CUs hold, the planner halves
     # the slice of x rows while that gives more workgroups; elsewhere the widest slice that fits
-    want = {(1, 4096, 4096): 1, (2, 6144, 4096): 1, (2, 4096, 4096): 1, (3, 6144, 4096): 2,
+    want = {(1, 6144, 4096): 1, (2, 6144, 4096): 1, (2, 4096, 4096): 1, (3, 6144, 4096): 2,
             (4, 6144, 4096): 2, (4, 4096, 4096): 2, (4, 28672, 4096): 4, (4, 4096, 14336): 4,
             (4, 128256, 4096): 4, (8, 6144, 4096): 4, (16, 6144, 4096): 8, (16, 28672, 4096): 8,
             (16, 4096, 14336): 4}
@@ -130,6 +130,14 @@ def test_skinny_slice_width():
         assert rg.rg_plan(64, 28672, 4096)["kernel_name"] == "ktile"
     finally:
         rg.rg_linear_set_launch(None)
+
+
+def test_one_row_kernel_choice():
+    # M = 1: the GEMV for K = 4096 on layers of at most 4096 rows, the skinny kernel elsewhere
+    for shape, name in (((1, 4096, 4096), "gemv"), ((1, 2048, 4096), "gemv"), ((1, 6144, 4096), "skinny"),
+                        ((1, 28672, 4096), "skinny"), ((1, 4096, 14336), "skinny"), ((1, 4096, 8192), "skinny"),
+                        ((1, 1024, 1024), "skinny"), ((2, 4096, 4096), "skinny")):
+        assert rg.rg_plan(*shape)["kernel_name"] == name, shape
 
 
 def test_mid_batch_kernel_choice():

@@ -28,7 +28,7 @@ def _check(M, N, K, seed=0, cfg=None, expect=None, bias=False):
     import torch
     import oracle
     import paper_2609_25624_amd as rg
-    if cfg:
+    if cfg is not None:
         rg.rg_linear_set_launch(kernel="skinny", **cfg)
     p = rg.rg_plan(M, N, K)
     assert p["kernel_name"] == "skinny", p
@@ -55,7 +55,8 @@ def _check(M, N, K, seed=0, cfg=None, expect=None, bias=False):
 @pytest.mark.parametrize("M", [1, 2, 3, 4, 8, 16])
 @pytest.mark.parametrize("N,K", [(6144, 4096), (4096, 4096), (28672, 4096), (4096, 14336)])
 def test_llama_decode_layers_full_output(M, N, K):
-    _check(M, N, K, seed=M * 7 + K)
+    # (the planner gives M = 1 on 4096 x 4096 to the GEMV; the skinny kernel is forced there)
+    _check(M, N, K, seed=M * 7 + K, cfg={} if M == 1 else None)
 
 
 @pytest.mark.parametrize("M", [1, 2, 4, 5, 9, 16])
