@@ -14,7 +14,7 @@ constexpr int wtile_lds_bytes(int waves) {
     return waves * 2 * 2 * kWtileK * (kWtileRows + 4) * 4 + kWtileRows * kWtileRows * 4;
 }
 
-// waves: 4 (the only build).  x [M][K] FP32, w [N][K] BF16 bits or FP32, y [M][N]; K % 8 == 0 (BF16)
+// waves: 4 (the planner's choice) or 8 (forced launches).  x [M][K] FP32, w [N][K] BF16 bits or FP32, y [M][N]; K % 8 == 0 (BF16)
 // or K % 4 == 0 (FP32), x and w 16-byte aligned.  Grid: ceil(M / 64) * ceil(N / 64) workgroups.
 hipError_t launch_wtile(const float* x, const uint16_t* w, const float* bias, float* y, int64_t M, int64_t N,
                         int64_t K, int waves, int reverse, hipStream_t stream);
