@@ -76,8 +76,9 @@ typedef enum {
     RG_KERNEL_TILED = 2,     /* larger M: register-tiled kernel, whole K per workgroup */
     RG_KERNEL_DECODE_XS = 3, /* M == 1 (when forced, or where the skinny kernel's x does not fit its
                                 registers): streaming GEMV with x streamed through LDS beside W */
-    RG_KERNEL_GEMV = 4,      /* M == 1, K % 256 == 0, K >= 4096 (when forced, or where the skinny
-                                kernel's x does not fit): 32 KB W bursts, whole rows per wave */
+    RG_KERNEL_GEMV = 4,      /* M == 1, K % 256 == 0, K >= 4096 (the default for K == 4096 with
+                                N <= 4096; elsewhere when forced, or where the skinny kernel's x
+                                does not fit): 32 KB W bursts, whole rows per wave */
     RG_KERNEL_STREAM = 5,    /* M <= 4: 8-row blocks of W streamed through LDS, one chain per lane
                                 (FP32 weights by default; BF16 weights when forced) */
     RG_KERNEL_KTILE = 6,     /* 16 < M <= 64 (any M when forced): 4 x 4 register tiles, K segments
