@@ -496,21 +496,29 @@ __global__ void __launch_bounds__(256) attn_partials_kernel(AttnArgs a) {
 // chains run over the valid positions only (the same values as chains over the
 // +0-padded segment).  INMAX: the wave takes its item's row maxima from the
 // segment maxima itself (the largest one per head, exact), so the maximum kernel
-// is not launched; used when no wave has more than one item.
-template <int G, int D, bool INMAX>
+// is not launched; used when no wave has more than one item.  CS = 2: the value
+// columns of an item are split between two waves (columns [0, D/2) and [D/2, D)),
+// each running the full chains of its columns (the same order: a chain is one
+// column's sum over the positions), for grids that would otherwise hold about one
+// wave per SIMD; with D = 128 a lane then owns one column.
+template <int G, int D, bool INMAX, int CS>
 __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
-    constexpr int RS = 4096 / D;                       // rows per step (8 KB of bf16)
-    constexpr int PPL = D / 128;                       // value pairs per lane
+    static_assert(CS == 1 || CS == 2, "column split");
+    constexpr int DH = D / CS;                         // value columns of this wave
+    constexpr int RS = 4096 / DH;                      // rows per step (8 KB of bf16)
+    constexpr int PPL = DH >= 128 ? DH / 128 : 0;      // value pairs per lane (0: one column)
     constexpr int GP = G <= 4 ? 4 : 8;                 // e row stride (floats)
-    constexpr int NVL = RS * D / 8 / 64;               // 16-byte vectors per lane per step (8)
+    constexpr int NVL = RS * DH / 8 / 64;              // 16-byte vectors per lane per step (8)
     constexpr int NTL = (RS * G + 63) / 64;            // scores per lane per step
-    __shared__ __attribute__((aligned(16))) uint16_t vs[4][RS * D];
+    constexpr int NC = PPL > 0 ? PPL : 1;              // chain sets per head
+    __shared__ __attribute__((aligned(16))) uint16_t vs[4][RS * DH];
     __shared__ __attribute__((aligned(16))) float es[4][RS * GP];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int items = (int)(a.B * a.Hkv * a.J);
-    const int tw = (int)gridDim.x * 4;                 // waves in the grid
-    const int gw = (int)blockIdx.x * 4 + wave;
+    const int tw = (int)gridDim.x * 4 / CS;            // waves in the grid per column half
+    const int gw = ((int)blockIdx.x * 4 + wave) / CS;
+    const int half = ((int)blockIdx.x * 4 + wave) % CS;   // 0 for CS = 1
     uint16_t* vw = vs[wave];
     float* ew = es[wave];
 
@@ -530,12 +538,12 @@ __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
     auto fetch = [&](const Item& w, int s) {
         const int r0 = s * RS;
         const int nrow = min(RS, w.rows - r0);          // >= 1
-        const uint16_t* vb = a.v + (((int64_t)w.b * a.Hkv + w.g) * a.Lmax + w.l0 + r0) * D;
+        const uint16_t* vb = a.v + (((int64_t)w.b * a.Hkv + w.g) * a.Lmax + w.l0 + r0) * D + half * DH;
 #pragma unroll
         for (int u = 0; u < NVL; ++u) {
-            const int i = lane + 64 * u;                // vector i: row i / (D / 8), column 8 (i % (D / 8))
-            const int row = i / (D / 8);
-            vr[u] = row < nrow ? ldnt(reinterpret_cast<const uint4*>(vb + (int64_t)row * D + 8 * (i % (D / 8))))
+            const int i = lane + 64 * u;                // vector i: row i / (DH / 8), column 8 (i % (DH / 8))
+            const int row = i / (DH / 8);
+            vr[u] = row < nrow ? ldnt(reinterpret_cast<const uint4*>(vb + (int64_t)row * D + 8 * (i % (DH / 8))))
                                : make_uint4(0u, 0u, 0u, 0u);
         }
         const int64_t tb = ((int64_t)w.b * a.H + (int64_t)w.g * G) * a.Lmax + w.l0 + r0;
@@ -582,7 +590,7 @@ __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
     Item w = item_of(a, it);
     int st = 0;
     fetch(w, 0);
-    float n0[PPL][G], n1[PPL][G], ssum = 0.0f;
+    float n0[NC][G], n1[NC][G], ssum = 0.0f;
     float mcur[G];
     while (it < items) {
         const Item cur = w;
@@ -646,7 +654,7 @@ __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
         if (it < items) fetch(w, st);
         if (ss == 0) {
 #pragma unroll
-            for (int k = 0; k < PPL; ++k)
+            for (int k = 0; k < NC; ++k)
 #pragma unroll
                 for (int h = 0; h < G; ++h) n0[k][h] = n1[k][h] = 0.0f;
             ssum = 0.0f;
@@ -657,14 +665,21 @@ __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
             float ev[G];
 #pragma unroll
             for (int h = 0; h < G; ++h) ev[h] = ew[l * GP + h];
+            if constexpr (PPL == 0) {
+                // one column per lane
+                const float v1 = __uint_as_float((uint32_t)vw[l * DH + lane] << 16);
 #pragma unroll
-            for (int k = 0; k < PPL; ++k) {
-                const uint32_t v2 = *reinterpret_cast<const uint32_t*>(vw + l * D + 128 * k + 2 * lane);
-                const float vlo = __uint_as_float(v2 << 16), vhi = __uint_as_float(v2 & 0xffff0000u);
+                for (int h = 0; h < G; ++h) n0[0][h] = __builtin_fmaf(ev[h], v1, n0[0][h]);
+            } else {
 #pragma unroll
-                for (int h = 0; h < G; ++h) {
-                    n0[k][h] = __builtin_fmaf(ev[h], vlo, n0[k][h]);
-                    n1[k][h] = __builtin_fmaf(ev[h], vhi, n1[k][h]);
+                for (int k = 0; k < PPL; ++k) {
+                    const uint32_t v2 = *reinterpret_cast<const uint32_t*>(vw + l * DH + 128 * k + 2 * lane);
+                    const float vlo = __uint_as_float(v2 << 16), vhi = __uint_as_float(v2 & 0xffff0000u);
+#pragma unroll
+                    for (int h = 0; h < G; ++h) {
+                        n0[k][h] = __builtin_fmaf(ev[h], vlo, n0[k][h]);
+                        n1[k][h] = __builtin_fmaf(ev[h], vhi, n1[k][h]);
+                    }
                 }
             }
             ssum = ssum + es_own[l * GP];               // lanes < G: head `lane`'s segment sum
@@ -672,14 +687,20 @@ __global__ void __launch_bounds__(256) attn_partials_wave_kernel(AttnArgs a) {
         if (ss == (cur.rows + RS - 1) / RS - 1) {
             const int64_t hb = (int64_t)cur.b * a.H + (int64_t)cur.g * G;
 #pragma unroll
-            for (int h = 0; h < G; ++h)
+            for (int h = 0; h < G; ++h) {
+                float* nb = a.npart + ((hb + h) * a.J + cur.j) * D + half * DH;
+                if constexpr (PPL == 0) {
+                    nb[lane] = n0[0][h];
+                } else {
 #pragma unroll
-                for (int k = 0; k < PPL; ++k) {
-                    float* np = a.npart + ((hb + h) * a.J + cur.j) * D + 128 * k + 2 * lane;
-                    np[0] = n0[k][h];
-                    np[1] = n1[k][h];
+                    for (int k = 0; k < PPL; ++k) {
+                        nb[128 * k + 2 * lane] = n0[k][h];
+                        nb[128 * k + 2 * lane + 1] = n1[k][h];
+                    }
                 }
-            if (lane < G) a.spart[(hb + lane) * a.J + cur.j] = ssum;
+            }
+            // (both halves sum the same e in the same order; the first writes the sums)
+            if (lane < G && half == 0) a.spart[(hb + lane) * a.J + cur.j] = ssum;
         }
         __builtin_amdgcn_wave_barrier();
     }
@@ -759,7 +780,9 @@ hipError_t launch_pair(K1 k1, int64_t lds1, K3 k3, int64_t lds3, const AttnArgs&
 // 111 -> 90 us for the scores of a 32 x 64-head, 4096-position batch, and 0-22 %
 // slower than the 64-column kernel with six or fewer heads).  Partials: one wave per
 // work item for D = 128 and 256 (four 4-wave workgroups per CU, each wave walking
-// items gw, gw + waves, ...); for D = 64 the workgroup-per-item kernel with
+// items gw, gw + waves, ...), two waves per item (value columns split) when there
+// are at most four items per CU (one 32K-token sequence: the pass 21.0 -> 20.3 us,
+// the call level within its spread); for D = 64 the workgroup-per-item kernel with
 // 16384 / D-row value steps (32 KB tiles, four workgroups per CU).  Other D <= DM:
 // launch_any.
 template <int G, int D>
@@ -781,8 +804,11 @@ hipError_t launch_fixed(const AttnArgs& a, int cus, hipStream_t stream) {
     // item the waves take the row maxima themselves and the maximum kernel is not launched
     // (measured 1-8 % faster with up to six query heads per kv head, 1 % slower with eight)
     constexpr bool kInmax = (D == 128 || D == 256) && G < 8;
-    const int64_t gw = (items + 3) / 4 < 4 * (int64_t)cus ? (items + 3) / 4 : 4 * (int64_t)cus;
-    const bool inmax = kInmax && items <= 4 * gw;
+    // at most one item per SIMD (one long sequence, say): each item's value columns are
+    // split between two waves
+    const int cs = (D == 128 || D == 256) && items <= 4 * (int64_t)cus ? 2 : 1;
+    const int64_t gw = (cs * items + 3) / 4 < 4 * (int64_t)cus ? (cs * items + 3) / 4 : 4 * (int64_t)cus;
+    const bool inmax = kInmax && cs * items <= 4 * gw;
     if (!inmax) {
         hipLaunchKernelGGL(attn_max_kernel, dim3((unsigned)((a.B * a.H + 255) / 256)), dim3(256), 0, stream, a);
         e = hipGetLastError();
@@ -792,12 +818,23 @@ hipError_t launch_fixed(const AttnArgs& a, int cus, hipStream_t stream) {
         bool launched = false;
         if constexpr (kInmax) {
             if (inmax) {
-                hipLaunchKernelGGL((attn_partials_wave_kernel<G, D, true>), dim3((unsigned)gw), dim3(256), 0, stream, a);
+                if (cs == 2)
+                    hipLaunchKernelGGL((attn_partials_wave_kernel<G, D, true, 2>), dim3((unsigned)gw), dim3(256), 0,
+                                       stream, a);
+                else
+                    hipLaunchKernelGGL((attn_partials_wave_kernel<G, D, true, 1>), dim3((unsigned)gw), dim3(256), 0,
+                                       stream, a);
                 launched = true;
             }
         }
-        if (!launched)
-            hipLaunchKernelGGL((attn_partials_wave_kernel<G, D, false>), dim3((unsigned)gw), dim3(256), 0, stream, a);
+        if (!launched) {
+            if (cs == 2)
+                hipLaunchKernelGGL((attn_partials_wave_kernel<G, D, false, 2>), dim3((unsigned)gw), dim3(256), 0, stream,
+                                   a);
+            else
+                hipLaunchKernelGGL((attn_partials_wave_kernel<G, D, false, 1>), dim3((unsigned)gw), dim3(256), 0, stream,
+                                   a);
+        }
     } else {
         const int64_t lds3 = (int64_t)G * kAttnSeg * 4 + (int64_t)RS * (D + 8) * 2;
         const int64_t g3 = items < (kLdsPerCU / lds3) * cus ? items : (kLdsPerCU / lds3) * cus;

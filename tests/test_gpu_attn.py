@@ -182,6 +182,22 @@ def test_both_row_maximum_paths():
     _assert_same(got2, got[:3], "first three sequences alone")
 
 
+@pytest.mark.parametrize("D", [128, 256])
+def test_whole_and_split_value_columns(D):
+    """More work items than four per CU: one wave takes all value columns of an item; the
+    first three sequences alone (few items): two waves split each item's columns.  Both
+    equal the oracle and each other."""
+    import paper_2609_25624_amd as rg
+    H, Hkv, Lmax = 4, 2, 1024
+    B = 4 * rg.rg_device_cu_count() // (Hkv * (Lmax // 256)) + 1
+    assert B * Hkv * (Lmax // 256) > 4 * rg.rg_device_cu_count()
+    assert 3 * Hkv * (Lmax // 256) <= 4 * rg.rg_device_cu_count()
+    lens = [1024 - 97 * (b % 11) for b in range(B)]
+    q, kc, vc, got = _check(B, H, Hkv, Lmax, D, lens, seed=31 + D)
+    got2 = _run(q[:3], kc[:3], vc[:3], lens[:3], np.float32(1.0 / np.sqrt(D)))
+    _assert_same(got2, got[:3], "first three sequences alone")
+
+
 @pytest.mark.parametrize("H,L", [(4, 33000), (3, 44000), (7, 19000)])
 def test_in_kernel_maximum_beyond_512_segment_maxima(H, L):
     """One sequence long enough that its G x Jb segment maxima exceed the 512 a wave loads with
